@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark of one GPU's share of a spatially decomposed 3x3 convolution layer.
+
+Workload (default): a 256x256 interior tile (tile (1,1)) of a 1024x1024 image on
+a 4x4 spatial grid, N=4 samples (this GPU's share of a 32-sample mini-batch),
+C=K=64, 3x3 stride 1 pad 1, halo width 1, bf16 inputs, fp32 accumulation and
+outputs -- hybrid sample/spatial parallelism (Sec. III-A) at the largest
+per-tile shape in the workload set.
+
+One step = the whole per-tile path of Sec. III-A on that tile:
+  halo pack x -> halo unpack x -> forward (Eq. 1) ->
+  halo pack dy -> halo unpack dy -> weight gradient (Eq. 2) -> input gradient (Eq. 3)
+The neighbours' halo regions (what the exchange would deliver) are prepared
+once before timing; the transport itself is not part of a GPU's compute.
+All inputs are resident in device memory when timing starts.
+
+value = (forward + backward-data + backward-filter flops) / step time, TFLOP/s.
+Prints one JSON line.  Only one GPU is supported (--gpus 1).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "conv fwd+bwd TFLOP/s and % MFMA peak per layer tile on 1 MI355X; halo GB/s"
+PEAK = {"bf16_tflops": 2516.6, "f32_tflops": 157.3, "hbm_gbps": 8000.0}
+
+
+def algorithmic(L):
+    """Compulsory HBM bytes and flops per launch of each pass on one tile.
+
+    Inputs in the layer dtype (x tile including its real halo margins, dy
+    interior, w), outputs in fp32, each read or written once."""
+    e = 2 if L.dtype == "bf16" else 4
+    h = L.halo
+    # real halo = margins that come from neighbours (interior tile: all four sides)
+    x_in = L.N * L.C * (L.Ht + 2 * h) * (L.Wt + 2 * h) * e
+    dy_in = L.N * L.K * (L.Hot + 2 * h) * (L.Wot + 2 * h) * e
+    dy_int = L.N * L.K * L.Hot * L.Wot * e
+    w = L.K * L.C * L.R * L.S * e
+    y = L.N * L.K * L.Hot * L.Wot * 4
+    dx = L.N * L.C * L.Ht * L.Wt * 4
+    dw = L.K * L.C * L.R * L.S * 4
+    flops = L.flops_per_pass_tile()
+    hx = L.N * L.C * (2 * h * (L.Ht + L.Wt) + 4 * h * h) * e
+    hy = L.N * L.K * (2 * h * (L.Hot + L.Wot) + 4 * h * h) * e
+    return {
+        "fwd": {"flops": flops, "bytes": x_in + w + y},
+        "bwd_data": {"flops": flops, "bytes": dy_in + w + dx},
+        "bwd_filter": {"flops": flops, "bytes": x_in + dy_int + dw},
+        "pack_x": {"flops": 0, "bytes": 2 * hx},
+        "unpack_x": {"flops": 0, "bytes": 2 * hx},
+        "pack_dy": {"flops": 0, "bytes": 2 * hy},
+        "unpack_dy": {"flops": 0, "bytes": 2 * hy},
+    }
+
+
+def cpu_baseline(L, x, w, dy, tile, seconds):
+    """The oracle, as it stands, on a bounded sample of the same tile's work."""
+    import numpy as np
+    import oracle as orc
+
+    ti, tj = divmod(tile, L.Q)
+    h = L.halo
+    lo, hi = L.pad, L.R - 1 - L.pad
+    win = orc.tile_window(x, L.P, L.Q, ti, tj, h)
+    xs = np.ascontiguousarray(win[:, :, h - lo:h + L.Ht + hi, h - lo:h + L.Wt + hi])
+    dwin = orc.tile_window(dy, L.P, L.Q, ti, tj, h)
+    dys = np.ascontiguousarray(dwin[:, :, h - hi:h + L.Hot + lo, h - hi:h + L.Wot + lo])
+    dyt = np.ascontiguousarray(dy[:, :, ti * L.Hot:(ti + 1) * L.Hot, tj * L.Wot:(tj + 1) * L.Wot])
+    rng = np.random.default_rng(7)
+    per_y = 2 * L.C * L.R * L.S
+    per_dx = 2 * L.K * L.R * L.S
+    per_dw = 2 * L.N * L.Hot * L.Wot
+
+    def run(kind, n):
+        if kind == "y":
+            idx = rng.integers(0, L.N * L.K * L.Hot * L.Wot, n)
+            t0 = time.perf_counter()
+            orc.conv_fwd_points(xs, w, 1, 0, idx)
+        elif kind == "dx":
+            idx = rng.integers(0, L.N * L.C * L.Ht * L.Wt, n)
+            t0 = time.perf_counter()
+            orc.conv_bwd_data_points(dys, w, L.Ht, L.Wt, 1, L.R - 1, idx)
+        else:
+            idx = rng.integers(0, L.K * L.C * L.R * L.S, n)
+            t0 = time.perf_counter()
+            orc.conv_bwd_filter_points(xs, dyt, L.R, L.S, 1, 0, idx)
+        return time.perf_counter() - t0
+
+    # calibrate, then give each pass a third of the budget
+    rate = {}
+    for kind, per, n in (("y", per_y, 4096), ("dx", per_dx, 4096), ("dw", per_dw, 16)):
+        dt = run(kind, n)
+        rate[kind] = n / max(dt, 1e-6)
+    total_flops, total_t, counts = 0, 0.0, {}
+    for kind, per in (("y", per_y), ("dx", per_dx), ("dw", per_dw)):
+        n = max(16, int(rate[kind] * seconds / 3))
+        dt = run(kind, n)
+        counts[kind] = n
+        total_flops += n * per
+        total_t += dt
+    return {
+        "value": total_flops / total_t / 1e12,
+        "unit": "TFLOP/s",
+        "cores": orc.num_threads(),
+        "kind": "oracle",
+        "sample": (f"{counts['y']} y, {counts['dx']} dx and {counts['dw']} dw outputs of tile "
+                   f"({ti},{tj}), fp64 direct loops, {total_t:.1f} s"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None, help="layer name in workloads.LAYERS")
+    ap.add_argument("--tile", type=int, default=None, help="tile index (default: an interior tile)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cold", action="store_true", help="also time steps after a cache flush")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU's tile; runs on more than one GPU are not supported "
+              "(use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import harness as H
+    import paper_1903_06681_amd as dc
+    import workloads as wl
+
+    L = wl.LAYERS[args.workload or wl.BENCH_LAYER]
+    p = dc.Problem.of(L)
+    nt = L.P * L.Q
+    tile = args.tile if args.tile is not None else (min(1, L.P - 1) * L.Q + min(1, L.Q - 1))
+    X, DY = dc.DC_X, dc.DC_DY
+    torch.cuda.set_device(0)
+    dev = "cuda"
+
+    # ---- inputs: global tensors, all tiles packed once, this tile's receive buffers
+    t_setup = time.perf_counter()
+    x, w, dy = wl.draw(L, "x"), wl.draw(L, "w"), wl.draw(L, "dy")
+    tdt = H.TORCH_DT[L.dtype]
+    xt = H.alloc_tiles(p, X, nt, L.dtype)
+    H.scatter_interiors(xt, H.to_device(x, L.dtype), p, X)
+    sx_all = torch.empty((nt, max(dc.halo_elems(p, X), 1)), dtype=tdt, device=dev)
+    dc.halo_pack(p, dc.DC_ALL_TILES, X, xt, sx_all)
+    xp = xt[tile].clone()
+    del xt
+    dyt = H.alloc_tiles(p, DY, nt, L.dtype)
+    H.scatter_interiors(dyt, H.to_device(dy, L.dtype), p, DY)
+    sy_all = torch.empty((nt, max(dc.halo_elems(p, DY), 1)), dtype=tdt, device=dev)
+    dc.halo_pack(p, dc.DC_ALL_TILES, DY, dyt, sy_all)
+    dyp = dyt[tile].clone()
+    del dyt
+    recv_x, recv_dy = torch.zeros_like(sx_all[0]), torch.zeros_like(sy_all[0])
+    H.exchange_into(recv_x, sx_all, p, X, tile)
+    H.exchange_into(recv_dy, sy_all, p, DY, tile)
+    del sx_all, sy_all
+    send_x, send_dy = torch.empty_like(recv_x), torch.empty_like(recv_dy)
+    wd = H.to_device(w, L.dtype)
+    y = torch.empty((L.N, L.K, L.Hot, L.Wot), device=dev)
+    dx = torch.empty((L.N, L.C, L.Ht, L.Wt), device=dev)
+    dw = torch.empty((L.K, L.C, L.R, L.S), device=dev)
+    ws = torch.empty(max(dc.bwd_filter_workspace_bytes(p, tile), 16), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t_setup
+
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    names = ["pack_x", "unpack_x", "fwd", "pack_dy", "unpack_dy", "bwd_filter", "bwd_data"]
+    calls = [
+        lambda: dc.halo_pack(p, tile, X, xp, send_x, sh),
+        lambda: dc.halo_unpack(p, tile, X, recv_x, xp, sh),
+        lambda: dc.conv_fwd(p, tile, xp, wd, y, sh),
+        lambda: dc.halo_pack(p, tile, DY, dyp, send_dy, sh),
+        lambda: dc.halo_unpack(p, tile, DY, recv_dy, dyp, sh),
+        lambda: dc.conv_bwd_filter(p, tile, xp, dyp, dw, 0, ws, sh),
+        lambda: dc.conv_bwd_data(p, tile, dyp, wd, dx, sh),
+    ]
+
+    def step(events=None):
+        for i, c in enumerate(calls):
+            if events is not None:
+                events[i].record(stream)
+            c()
+        if events is not None:
+            events[len(calls)].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+          for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for k in range(args.steps):
+        step(ev[k])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_per_step = total_ms / args.steps
+    per_call = {n: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
+                for i, n in enumerate(names)}
+
+    alg = algorithmic(L)
+    flops_step = 3 * L.flops_per_pass_tile()
+    value = flops_step / (ms_per_step * 1e-3) / 1e12
+    peak_tf = PEAK["bf16_tflops"] if L.dtype == "bf16" else PEAK["f32_tflops"]
+    ridge = peak_tf * 1e12 / (PEAK["hbm_gbps"] * 1e9)
+    passes = {}
+    for n in names:
+        ms = per_call[n]
+        a = alg[n]
+        d = {"ms": round(ms, 5), "bytes": a["bytes"],
+             "GB/s": round(a["bytes"] / (ms * 1e-3) / 1e9, 1)}
+        if a["flops"]:
+            d["flops"] = a["flops"]
+            d["TFLOP/s"] = round(a["flops"] / (ms * 1e-3) / 1e12, 2)
+            d["pct_mfma_peak"] = round(100 * d["TFLOP/s"] / peak_tf, 2)
+            ai = a["flops"] / a["bytes"]
+            roof = min(peak_tf, ai * PEAK["hbm_gbps"] / 1e3)
+            d["roof_TFLOP/s"] = round(roof, 1)
+            d["pct_roof"] = round(100 * d["TFLOP/s"] / roof, 2)
+        passes[n] = d
+    dom = max(("fwd", "bwd_data", "bwd_filter"), key=lambda n: per_call[n])
+    a = alg[dom]
+    ai = a["flops"] / a["bytes"]
+    if ai < ridge:
+        ach = a["bytes"] / (per_call[dom] * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK["hbm_gbps"],
+                    "unit": "GB/s", "frac": round(ach / PEAK["hbm_gbps"], 4), "traffic": None}
+    else:
+        ach = a["flops"] / (per_call[dom] * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak_tf,
+                    "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4), "traffic": None}
+    roofline["kernel"] = {"fwd": "dc_conv_fwd", "bwd_data": "dc_conv_bwd_data",
+                          "bwd_filter": "dc_conv_bwd_filter"}[dom]
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": L.dtype,
+        "data": "synthetic (seeded uniform/normal inputs of the paper's layer shapes)",
+        "config": {"workload": f"{L.name}: {L.desc}", "tile": tile, "N": L.N, "C": L.C, "K": L.K,
+                   "H": L.H, "W": L.W, "R": L.R, "S": L.S, "stride": L.stride, "pad": L.pad,
+                   "grid": f"{L.P}x{L.Q}", "halo": L.halo, "global_batch": L.N,
+                   "parallelism": "one spatial tile (hybrid sample/spatial)"},
+        "roofline": roofline,
+        "passes": passes,
+        "halo_GB/s": {n: passes[n]["GB/s"] for n in ("pack_x", "unpack_x", "pack_dy", "unpack_dy")},
+        "setup_s": round(t_setup, 1),
+    }
+
+    if args.cold:
+        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+        cold = []
+        for _ in range(min(args.steps, 10)):
+            flush.zero_()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            cold.append(e0.elapsed_time(e1))
+        out["cold_ms_per_step"] = round(float(np.mean(cold)), 5)
+        del flush
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(L, x, w, dy, tile, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

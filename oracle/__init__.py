@@ -58,8 +58,15 @@ def _load():
                  "oracle_conv_bwd_filter_points"):
         getattr(lib, name).argtypes = dims + [_PF, _PF, _PI, _I64, _PD]
         getattr(lib, name).restype = None
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's loops run on."""
+    return int(_load().oracle_num_threads())
 
 
 def _f32(a) -> np.ndarray:

@@ -35,6 +35,7 @@
  */
 #include <stdint.h>
 #include <stddef.h>
+#include <omp.h>
 
 typedef int64_t i64;
 
@@ -184,3 +185,6 @@ void oracle_conv_bwd_filter_points(i64 N, i64 C, i64 K, i64 Hi, i64 Wi, i64 Ho, 
         out[t] = bwd_filter_one(x, dy, N, C, K, Hi, Wi, Ho, Wo, stride, pad, f, c, r, s);
     }
 }
+
+/* Threads the OpenMP loops above use (for reporting timings). */
+int oracle_num_threads(void) { return omp_get_max_threads(); }

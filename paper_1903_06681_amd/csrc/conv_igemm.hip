@@ -1,0 +1,355 @@
+// Forward and backward-data convolution on a padded tile as an implicit GEMM
+// on gfx950 matrix cores (Eqs. (1) and (3) of Sec. II-A on the tile of
+// Sec. III-A).
+//
+//   D[o][pixel] = sum_{kg} A[o][kg] * B[kg][pixel],  kg = (tap, input channel)
+//
+// A is the weight tensor, B the implicit im2col view of the padded input
+// tile.  A workgroup of 4 waves computes OB output channels x (4 rows x 64
+// columns) of output pixels; wave w owns output row w, as OB/32 x 2 MFMA
+// 32x32 tiles.  The input channels are walked in chunks of CC: each chunk
+// stages the weights [tap, 8-channel group][o][8] and the input patch
+// (rows x cols x channels, channel-innermost) in LDS, then runs the MFMA loop.
+//
+// bf16: v_mfma_f32_32x32x16_bf16.  A k-step of 16 = two groups of 8 channels
+//       (one per half-wave), each group at its own tap; the 8 channels of a
+//       pixel are one 16-byte LDS read.  The NCHW -> channel-innermost
+//       transpose happens while staging.
+// fp32: v_mfma_f32_32x32x2_f32.  A k-step of 2 = one (tap, channel) per
+//       half-wave; a lane reads one float, so the patch stays channel-major.
+// Accumulation is fp32 in both; outputs are fp32 stores of 32 consecutive
+// pixels per half-wave (128-byte segments).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace dc {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
+
+static constexpr int kThreads = 256;
+static constexpr int kBH = 4;    // output rows per workgroup (one per wave)
+static constexpr int kBW = 64;   // output columns per workgroup (two 32-pixel MFMA tiles)
+
+// Pixel stride (bf16 elements) of the channel-innermost patch: an odd number
+// of 16-byte units, so 16 consecutive lanes reading 16 B each hit distinct
+// bank groups.
+__host__ __device__ inline int bf16_pixel_stride(int CC) { return 8 * ((CC / 8) | 1); }
+
+// fp32 patch plane stride (floats): rows*cols rounded up to 32 mod 64, so the
+// two half-waves (adjacent channels, same pixels) use disjoint banks.
+__host__ __device__ inline int f32_plane_stride(int PR, int PC) {
+    int p = PR * PC;
+    int r = p % 64;
+    return r <= 32 ? p + (32 - r) : p + (96 - r);
+}
+
+union Pack8 {
+    uint4 v;
+    uint16_t h[8];
+};
+
+template <int OB>
+__global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int NOB = OB / 32;
+    const int CC = a.CC, CCG = CC / 8;
+    const int Tt = a.Tr * a.Ts;
+    const int G = Tt * CCG;
+    const int PR = (kBH - 1) * a.istr + a.Tr;
+    const int PC = (kBW - 1) * a.istr + a.Ts;
+    const int PS = bf16_pixel_stride(CC);
+    uint16_t* wl = reinterpret_cast<uint16_t*>(smem);   // [G][OB][8]
+    uint16_t* pl = wl + G * OB * 8;                      // [PR][PC][PS]
+
+    const int nvb = (a.Vo + kBW - 1) / kBW;
+    const int vb = blockIdx.x % nvb, ub = blockIdx.x / nvb;
+    const int o0 = blockIdx.y * OB;
+    const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
+    const int u0 = ub * kBH, v0 = vb * kBW;
+
+    const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
+    const uint16_t* in = static_cast<const uint16_t*>(a.in) + tile * a.in_tile +
+                         int64_t(n) * a.Cin * plane;
+    const uint16_t* w = static_cast<const uint16_t*>(a.w);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int row_in0 = u0 * a.istr + a.base_r;
+    const int col_in0 = v0 * a.istr + a.base_c;
+
+    floatx16 acc[NOB][2];
+#pragma unroll
+    for (int i = 0; i < NOB; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    for (int c0 = 0; c0 < a.Cin; c0 += CC) {
+        __syncthreads();
+        // weights: one 8-channel vector per (group, output channel)
+        for (int e = tid; e < G * OB; e += kThreads) {
+            const int g = e / OB, ol = e - g * OB;
+            const int t = g / CCG, cb = g - t * CCG;
+            const int tr = t / a.Ts, ts = t - tr * a.Ts;
+            const int o = o0 + ol;
+            const int wr = a.wr0 + a.wrstep * tr, ws = a.ws0 + a.wsstep * ts;
+            Pack8 p;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int ci = c0 + cb * 8 + j;
+                p.h[j] = (o < a.Cout && ci < a.Cin)
+                             ? w[o * a.w_os + ci * a.w_cs + wr * a.S + ws]
+                             : uint16_t(0);
+            }
+            *reinterpret_cast<uint4*>(wl + e * 8) = p.v;
+        }
+        // input patch, transposed to channel-innermost
+        for (int e = tid; e < PR * CCG * PC; e += kThreads) {
+            const int pc = e % PC;
+            const int rest = e / PC;
+            const int cg = rest % CCG, pr = rest / CCG;
+            const int gr = row_in0 + pr, gc = col_in0 + pc;
+            const bool ok = gr >= 0 && gr < a.in_rows && gc >= 0 && gc < a.in_cols;
+            const uint16_t* src = in + int64_t(gr) * a.in_pitch + gc;
+            Pack8 p;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int ci = c0 + cg * 8 + j;
+                p.h[j] = (ok && ci < a.Cin) ? src[int64_t(ci) * plane] : uint16_t(0);
+            }
+            *reinterpret_cast<uint4*>(pl + (pr * PC + pc) * PS + cg * 8) = p.v;
+        }
+        __syncthreads();
+
+        const int nk = (G + 1) / 2;
+        for (int k = 0; k < nk; ++k) {
+            const int g = 2 * k + hi;
+            bf16x8 A[NOB], B[2];
+            if (g < G) {
+                const int t = g / CCG, cb = g - t * CCG;
+                const int tr = t / a.Ts, ts = t - tr * a.Ts;
+#pragma unroll
+                for (int ob = 0; ob < NOB; ++ob)
+                    A[ob] = *reinterpret_cast<const bf16x8*>(wl + (g * OB + ob * 32 + l32) * 8);
+                const int prow = wave * a.istr + tr;
+#pragma unroll
+                for (int pb = 0; pb < 2; ++pb) {
+                    const int pcol = (pb * 32 + l32) * a.istr + ts;
+                    B[pb] = *reinterpret_cast<const bf16x8*>(pl + (prow * PC + pcol) * PS + cb * 8);
+                }
+            } else {
+#pragma unroll
+                for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) A[ob][j] = __bf16(0.f);
+#pragma unroll
+                for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) B[pb][j] = __bf16(0.f);
+            }
+#pragma unroll
+            for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+                for (int pb = 0; pb < 2; ++pb)
+                    acc[ob][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[ob], B[pb], acc[ob][pb], 0, 0, 0);
+        }
+    }
+
+    // D layout of a 32x32 MFMA tile: value i of lane l is row 8*(i/4) + 4*(l/32) + i%4,
+    // column l%32.  Rows are output channels, columns pixels.
+    const int u = u0 + wave;
+    if (u >= a.Uo) return;
+    float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
+    const int orow = u * a.ostr + a.oph_r;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+            const int v = v0 + pb * 32 + l32;
+            if (v >= a.Vo) continue;
+            const int ocol = v * a.ostr + a.oph_c;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int o = o0 + ob * 32 + 8 * (i / 4) + 4 * hi + (i % 4);
+                if (o < a.Cout)
+                    out[(int64_t(o) * a.out_rows + orow) * a.out_cols + ocol] = acc[ob][pb][i];
+            }
+        }
+}
+
+template <int OB>
+__global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int NOB = OB / 32;
+    const int CC = a.CC;
+    const int Tt = a.Tr * a.Ts;
+    const int KG = Tt * CC;
+    const int PR = (kBH - 1) * a.istr + a.Tr;
+    const int PC = (kBW - 1) * a.istr + a.Ts;
+    const int PLN = f32_plane_stride(PR, PC);
+    float* wl = reinterpret_cast<float*>(smem);   // [KG][OB]
+    float* pl = wl + KG * OB;                     // [CC][PLN] with rows of PC
+
+    const int nvb = (a.Vo + kBW - 1) / kBW;
+    const int vb = blockIdx.x % nvb, ub = blockIdx.x / nvb;
+    const int o0 = blockIdx.y * OB;
+    const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
+    const int u0 = ub * kBH, v0 = vb * kBW;
+
+    const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
+    const float* in = static_cast<const float*>(a.in) + tile * a.in_tile +
+                      int64_t(n) * a.Cin * plane;
+    const float* w = static_cast<const float*>(a.w);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int row_in0 = u0 * a.istr + a.base_r;
+    const int col_in0 = v0 * a.istr + a.base_c;
+
+    floatx16 acc[NOB][2];
+#pragma unroll
+    for (int i = 0; i < NOB; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    for (int c0 = 0; c0 < a.Cin; c0 += CC) {
+        __syncthreads();
+        for (int e = tid; e < KG * OB; e += kThreads) {
+            const int kg = e / OB, ol = e - kg * OB;
+            const int t = kg / CC, cl = kg - t * CC;
+            const int tr = t / a.Ts, ts = t - tr * a.Ts;
+            const int o = o0 + ol, ci = c0 + cl;
+            const int wr = a.wr0 + a.wrstep * tr, ws = a.ws0 + a.wsstep * ts;
+            wl[e] = (o < a.Cout && ci < a.Cin) ? w[o * a.w_os + ci * a.w_cs + wr * a.S + ws] : 0.f;
+        }
+        for (int e = tid; e < CC * PR * PC; e += kThreads) {
+            const int pc = e % PC;
+            const int rest = e / PC;
+            const int pr = rest % PR, cl = rest / PR;
+            const int gr = row_in0 + pr, gc = col_in0 + pc, ci = c0 + cl;
+            const bool ok = gr >= 0 && gr < a.in_rows && gc >= 0 && gc < a.in_cols && ci < a.Cin;
+            pl[cl * PLN + pr * PC + pc] = ok ? in[int64_t(ci) * plane + int64_t(gr) * a.in_pitch + gc] : 0.f;
+        }
+        __syncthreads();
+
+        const int nk = (KG + 1) / 2;
+        for (int k = 0; k < nk; ++k) {
+            const int kg = 2 * k + hi;
+            float A[NOB], B[2];
+            if (kg < KG) {
+                const int t = kg / CC, cl = kg - t * CC;
+                const int tr = t / a.Ts, ts = t - tr * a.Ts;
+#pragma unroll
+                for (int ob = 0; ob < NOB; ++ob) A[ob] = wl[kg * OB + ob * 32 + l32];
+                const int prow = wave * a.istr + tr;
+#pragma unroll
+                for (int pb = 0; pb < 2; ++pb)
+                    B[pb] = pl[cl * PLN + prow * PC + (pb * 32 + l32) * a.istr + ts];
+            } else {
+#pragma unroll
+                for (int ob = 0; ob < NOB; ++ob) A[ob] = 0.f;
+                B[0] = B[1] = 0.f;
+            }
+#pragma unroll
+            for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+                for (int pb = 0; pb < 2; ++pb)
+                    acc[ob][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(A[ob], B[pb], acc[ob][pb], 0, 0, 0);
+        }
+    }
+
+    const int u = u0 + wave;
+    if (u >= a.Uo) return;
+    float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
+    const int orow = u * a.ostr + a.oph_r;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+            const int v = v0 + pb * 32 + l32;
+            if (v >= a.Vo) continue;
+            const int ocol = v * a.ostr + a.oph_c;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int o = o0 + ob * 32 + 8 * (i / 4) + 4 * hi + (i % 4);
+                if (o < a.Cout)
+                    out[(int64_t(o) * a.out_rows + orow) * a.out_cols + ocol] = acc[ob][pb][i];
+            }
+        }
+}
+
+static int lds_bytes_for(const IgemmArgs& a, int dtype, int CC, int OB) {
+    const int PR = (kBH - 1) * a.istr + a.Tr;
+    const int PC = (kBW - 1) * a.istr + a.Ts;
+    const int Tt = a.Tr * a.Ts;
+    if (dtype == 1) {
+        const int G = Tt * (CC / 8);
+        return G * OB * 16 + PR * PC * bf16_pixel_stride(CC) * 2;
+    }
+    return (Tt * CC * OB + CC * f32_plane_stride(PR, PC)) * 4;
+}
+
+bool igemm_plan(IgemmArgs& a, int dtype) {
+    a.OB = a.Cout <= 32 ? 32 : 64;
+    // channel-chunk candidates, widest first: the channel count itself (rounded
+    // to the k-granularity) when it is small, then powers of two
+    const int gran = dtype == 1 ? 8 : 2;
+    const int maxcc = dtype == 1 ? 64 : 32;
+    const int cin_r = (a.Cin + gran - 1) / gran * gran;
+    int cands[8], nc = 0;
+    cands[nc++] = std::min(cin_r, maxcc);
+    for (int c = maxcc; c >= gran; c /= 2)
+        if (c < cands[0]) cands[nc++] = c;
+    // prefer two workgroups per CU (<= 80 KB of LDS), else the device limit
+    const int limit = device_lds_limit();
+    for (int budget : {std::min(80 * 1024, limit), limit}) {
+        for (int i = 0; i < nc; ++i) {
+            const int b = lds_bytes_for(a, dtype, cands[i], a.OB);
+            if (b <= budget) {
+                a.CC = cands[i];
+                a.lds_bytes = b;
+                return true;
+            }
+        }
+    }
+    return false;
+}
+
+hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
+    const int nvb = (a.Vo + kBW - 1) / kBW, nub = (a.Uo + kBH - 1) / kBH;
+    dim3 grid(nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
+    dim3 block(kThreads);
+    if (a.lds_bytes > 64 * 1024) {
+        hipError_t e = hipSuccess;
+        if (dtype == 1)
+            e = a.OB == 32 ? hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_bf16_kernel<32>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes)
+                           : hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_bf16_kernel<64>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
+        else
+            e = a.OB == 32 ? hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_f32_kernel<32>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes)
+                           : hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_f32_kernel<64>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
+        if (e != hipSuccess) return e;
+    }
+    if (dtype == 1) {
+        if (a.OB == 32)
+            hipLaunchKernelGGL(igemm_bf16_kernel<32>, grid, block, a.lds_bytes, s, a);
+        else
+            hipLaunchKernelGGL(igemm_bf16_kernel<64>, grid, block, a.lds_bytes, s, a);
+    } else {
+        if (a.OB == 32)
+            hipLaunchKernelGGL(igemm_f32_kernel<32>, grid, block, a.lds_bytes, s, a);
+        else
+            hipLaunchKernelGGL(igemm_f32_kernel<64>, grid, block, a.lds_bytes, s, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace dc

@@ -1,0 +1,386 @@
+// C entry points of libdc: argument validation, tile geometry and kernel
+// dispatch.  No allocation, no state, no synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+
+#include "dc.h"
+#include "geometry.h"
+#include "kernels.h"
+
+namespace dc {
+
+static const int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+static int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+// Margins Eq. (1) reads around a tile of `t_in` input / `t_out` output
+// positions along one axis: output positions p read inputs p*stride-pad+r.
+static void x_margins(int t_in, int t_out, int R, int stride, int pad, int* lo, int* hi) {
+    *lo = pad;
+    int last = (t_out - 1) * stride - pad + R - 1;   // furthest input read
+    *hi = std::max(0, last - (t_in - 1));
+}
+
+// Margins Eq. (3) reads around a tile: input position i reads output
+// positions (i+pad-r)/stride where the division is exact.
+static void dy_margins(int t_in, int t_out, int R, int stride, int pad, int* lo, int* hi) {
+    int64_t mmin = ceil_div(int64_t(pad) - (R - 1), stride);
+    int64_t mmax = floor_div(int64_t(t_in) - 1 + pad, stride);
+    *lo = int(std::max<int64_t>(0, -mmin));
+    *hi = int(std::max<int64_t>(0, mmax - (t_out - 1)));
+}
+
+dc_status make_geo(const dc_problem* p, Geo* g) {
+    if (!p || !g) return DC_ERR_NULL;
+    std::memset(g, 0, sizeof(*g));
+    if (p->N < 1 || p->C < 1 || p->K < 1 || p->H < 1 || p->W < 1 || p->R < 1 || p->S < 1 ||
+        p->stride < 1 || p->pad < 0 || p->P < 1 || p->Q < 1 || p->halo < 0)
+        return DC_ERR_SHAPE;
+    if (p->dtype != DC_F32 && p->dtype != DC_BF16) return DC_ERR_DTYPE;
+    g->N = p->N; g->C = p->C; g->K = p->K; g->H = p->H; g->W = p->W;
+    g->R = p->R; g->S = p->S; g->stride = p->stride; g->pad = p->pad;
+    g->P = p->P; g->Q = p->Q; g->h = p->halo; g->dtype = p->dtype;
+    g->esize = p->dtype == DC_BF16 ? 2 : 4;
+
+    int64_t ho = floor_div(int64_t(p->H) + 2 * int64_t(p->pad) - p->R, p->stride) + 1;
+    int64_t wo = floor_div(int64_t(p->W) + 2 * int64_t(p->pad) - p->S, p->stride) + 1;
+    if (ho < 1 || wo < 1) return DC_ERR_SHAPE;
+    g->Ho = int(ho); g->Wo = int(wo);
+    if (p->H % p->P != 0 || p->W % p->Q != 0) return DC_ERR_UNSUPPORTED;
+    g->ntiles = p->P * p->Q;
+    if (g->ntiles > 1) {
+        // Decomposed layers: stride 1 and "same" output, so output tiles
+        // coincide with input tiles (Sec. III-A's setting).
+        if (p->stride != 1 || g->Ho != p->H || g->Wo != p->W) return DC_ERR_UNSUPPORTED;
+    }
+    g->Ht = p->H / p->P; g->Wt = p->W / p->Q;
+    g->Hot = g->Ho / p->P; g->Wot = g->Wo / p->Q;
+
+    x_margins(g->Ht, g->Hot, p->R, p->stride, p->pad, &g->need_x_lo_r, &g->need_x_hi_r);
+    x_margins(g->Wt, g->Wot, p->S, p->stride, p->pad, &g->need_x_lo_s, &g->need_x_hi_s);
+    dy_margins(g->Ht, g->Hot, p->R, p->stride, p->pad, &g->need_dy_lo_r, &g->need_dy_hi_r);
+    dy_margins(g->Wt, g->Wot, p->S, p->stride, p->pad, &g->need_dy_lo_s, &g->need_dy_hi_s);
+    int need = std::max({g->need_x_lo_r, g->need_x_hi_r, g->need_x_lo_s, g->need_x_hi_s,
+                         g->need_dy_lo_r, g->need_dy_hi_r, g->need_dy_lo_s, g->need_dy_hi_s});
+    if (g->h < need) return DC_ERR_HALO;
+    // halos come from the adjacent tile only
+    if ((p->P > 1 && g->h > g->Ht) || (p->Q > 1 && g->h > g->Wt)) return DC_ERR_HALO;
+
+    const int align = 16 / g->esize;
+    g->x_rows = g->Ht + 2 * g->h;  g->x_cols = g->Wt + 2 * g->h;
+    g->dy_rows = g->Hot + 2 * g->h; g->dy_cols = g->Wot + 2 * g->h;
+    g->x_pitch = round_up(g->x_cols, align);
+    g->dy_pitch = round_up(g->dy_cols, align);
+    g->x_tile = int64_t(g->N) * g->C * g->x_rows * g->x_pitch;
+    g->dy_tile = int64_t(g->N) * g->K * g->dy_rows * g->dy_pitch;
+    int64_t hx = 2 * int64_t(g->h) * (g->Ht + g->Wt) + 4 * int64_t(g->h) * g->h;
+    int64_t hy = 2 * int64_t(g->h) * (g->Hot + g->Wot) + 4 * int64_t(g->h) * g->h;
+    g->x_halo = int64_t(g->N) * g->C * hx;
+    g->dy_halo = int64_t(g->N) * g->K * hy;
+    int64_t y_tile = int64_t(g->N) * g->K * g->Hot * g->Wot;
+    int64_t dx_tile = int64_t(g->N) * g->C * g->Ht * g->Wt;
+    int64_t w_elems = int64_t(g->K) * g->C * g->R * g->S;
+    if (g->x_tile > kMaxElems || g->dy_tile > kMaxElems || y_tile > kMaxElems ||
+        dx_tile > kMaxElems || w_elems > kMaxElems)
+        return DC_ERR_TOO_LARGE;
+    return DC_OK;
+}
+
+dc_status make_geo_tile(const dc_problem* p, int32_t tile, Geo* g) {
+    dc_status st = make_geo(p, g);
+    if (st != DC_OK) return st;
+    if (tile != DC_ALL_TILES && (tile < 0 || tile >= g->ntiles)) return DC_ERR_TILE;
+    return DC_OK;
+}
+
+int device_lds_limit() {
+    // per-device cache; a benign race at worst re-queries the same value
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 64 * 1024;
+    if (cache[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+            v <= 0)
+            v = 64 * 1024;
+        cache[dev] = v;
+    }
+    return cache[dev];
+}
+
+static bool misaligned(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) != 0; }
+
+static dc_status launched(hipError_t e) {
+    if (e != hipSuccess) return DC_ERR_HIP;
+    return hipGetLastError() == hipSuccess ? DC_OK : DC_ERR_HIP;
+}
+
+// ---------------------------------------------------------------- halo
+
+// Region table of the packed halo format: order N, S, W, E, NW, NE, SW, SE.
+static void halo_regions(int Ht, int Wt, int h, int planes, bool unpack, HaloRegion reg[8]) {
+    static const int di[8] = {-1, 1, 0, 0, -1, -1, 1, 1};
+    static const int dj[8] = {0, 0, -1, 1, -1, 1, -1, 1};
+    static const int opp[8] = {1, 0, 3, 2, 7, 6, 5, 4};
+    int64_t off = 0;
+    for (int d = 0; d < 8; ++d) {
+        HaloRegion& r = reg[d];
+        r.rows = di[d] == 0 ? Ht : h;
+        r.cols = dj[d] == 0 ? Wt : h;
+        r.off = off;
+        off += int64_t(planes) * r.rows * r.cols;
+        r.di = di[d]; r.dj = dj[d]; r.opp = opp[d];
+        if (!unpack) {  // band of the owned block next to neighbour d
+            r.tr0 = di[d] < 0 ? h : (di[d] > 0 ? Ht : h);
+            r.tc0 = dj[d] < 0 ? h : (dj[d] > 0 ? Wt : h);
+        } else {        // margin on side d
+            r.tr0 = di[d] < 0 ? 0 : (di[d] > 0 ? h + Ht : h);
+            r.tc0 = dj[d] < 0 ? 0 : (dj[d] > 0 ? h + Wt : h);
+        }
+    }
+}
+
+static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which,
+                             const void* src, void* dst, bool unpack, void* stream) {
+    Geo g;
+    dc_status st = make_geo_tile(prob, tile, &g);
+    if (st != DC_OK) return st;
+    if (which != DC_X && which != DC_DY) return DC_ERR_ARG;
+    const bool x = which == DC_X;
+    const int ch = x ? g.C : g.K;
+    const int Ht = x ? g.Ht : g.Hot, Wt = x ? g.Wt : g.Wot;
+    if (g.h == 0) return DC_OK;  // K = 1: no halo (Sec. III-A)
+    if (!src || !dst) return DC_ERR_NULL;
+    if (misaligned(src) || misaligned(dst)) return DC_ERR_ALIGN;
+    HaloArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.src = src; a.dst = dst;
+    a.tile_elems = x ? g.x_tile : g.dy_tile;
+    a.halo_elems = x ? g.x_halo : g.dy_halo;
+    a.planes = g.N * ch;
+    a.rows = x ? g.x_rows : g.dy_rows;
+    a.pitch = x ? g.x_pitch : g.dy_pitch;
+    a.P = g.P; a.Q = g.Q;
+    a.all_tiles = tile == DC_ALL_TILES;
+    a.tile0 = a.all_tiles ? 0 : tile;
+    a.ntiles = a.all_tiles ? g.ntiles : 1;
+    halo_regions(Ht, Wt, g.h, a.planes, unpack, a.reg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return launched(unpack ? launch_halo_unpack(a, g.esize, s) : launch_halo_pack(a, g.esize, s));
+}
+
+// ---------------------------------------------------------------- convs
+
+static void igemm_common(const Geo& g, int32_t tile, IgemmArgs& a) {
+    std::memset(&a, 0, sizeof(a));
+    a.ntiles = tile == DC_ALL_TILES ? g.ntiles : 1;
+    a.Nn = g.N;
+    a.S = g.S;
+}
+
+}  // namespace dc
+
+using namespace dc;
+
+extern "C" {
+
+dc_status dc_validate(const dc_problem* prob, int32_t tile) {
+    Geo g;
+    return make_geo_tile(prob, tile, &g);
+}
+
+int64_t dc_tile_pitch(const dc_problem* prob, int32_t which) {
+    Geo g;
+    if (make_geo(prob, &g) != DC_OK || (which != DC_X && which != DC_DY)) return -1;
+    return which == DC_X ? g.x_pitch : g.dy_pitch;
+}
+
+int64_t dc_tile_elems(const dc_problem* prob, int32_t which) {
+    Geo g;
+    if (make_geo(prob, &g) != DC_OK || (which != DC_X && which != DC_DY)) return -1;
+    return which == DC_X ? g.x_tile : g.dy_tile;
+}
+
+int64_t dc_halo_elems(const dc_problem* prob, int32_t which) {
+    Geo g;
+    if (make_geo(prob, &g) != DC_OK || (which != DC_X && which != DC_DY)) return -1;
+    return which == DC_X ? g.x_halo : g.dy_halo;
+}
+
+dc_status dc_required_halo(const dc_problem* prob, int32_t which, int32_t lohi[2]) {
+    if (!lohi) return DC_ERR_NULL;
+    dc_problem q;
+    if (!prob) return DC_ERR_NULL;
+    q = *prob;
+    // the requirement does not depend on the halo field: evaluate with a
+    // margin wide enough to pass the width check
+    q.halo = std::max(std::max(q.R, q.S) + q.pad, 0);
+    Geo g;
+    dc_status st = make_geo(&q, &g);
+    if (st != DC_OK && st != DC_ERR_HALO) return st;
+    if (st == DC_ERR_HALO) {
+        // tile narrower than the probe margin: recompute the margins directly
+        q.halo = 0;
+        st = make_geo(&q, &g);
+        if (st != DC_OK && st != DC_ERR_HALO) return st;
+    }
+    if (which == DC_X) {
+        lohi[0] = std::max(g.need_x_lo_r, g.need_x_lo_s);
+        lohi[1] = std::max(g.need_x_hi_r, g.need_x_hi_s);
+    } else if (which == DC_DY) {
+        lohi[0] = std::max(g.need_dy_lo_r, g.need_dy_lo_s);
+        lohi[1] = std::max(g.need_dy_hi_r, g.need_dy_hi_s);
+    } else {
+        return DC_ERR_ARG;
+    }
+    return DC_OK;
+}
+
+dc_status dc_tile_dims(const dc_problem* prob, int32_t dims[4]) {
+    if (!dims) return DC_ERR_NULL;
+    Geo g;
+    dc_status st = make_geo(prob, &g);
+    if (st != DC_OK) return st;
+    dims[0] = g.Ht; dims[1] = g.Wt; dims[2] = g.Hot; dims[3] = g.Wot;
+    return DC_OK;
+}
+
+const char* dc_status_string(int32_t s) {
+    switch (s) {
+        case DC_OK: return "ok";
+        case DC_ERR_NULL: return "null pointer";
+        case DC_ERR_SHAPE: return "invalid shape";
+        case DC_ERR_DTYPE: return "invalid dtype";
+        case DC_ERR_HALO: return "halo width does not fit the layer or the tiles";
+        case DC_ERR_UNSUPPORTED: return "unsupported decomposition";
+        case DC_ERR_WORKSPACE: return "workspace missing or too small";
+        case DC_ERR_ALIGN: return "device pointer not 16-byte aligned";
+        case DC_ERR_HIP: return "HIP runtime error";
+        case DC_ERR_TILE: return "tile index out of range";
+        case DC_ERR_ARG: return "invalid argument";
+        case DC_ERR_TOO_LARGE: return "tensor too large for 32-bit element indexing";
+        default: return "unknown status";
+    }
+}
+
+dc_status dc_halo_pack(const dc_problem* prob, int32_t tile, int32_t which,
+                       const void* t_pad, void* send, void* stream) {
+    return halo_common(prob, tile, which, t_pad, send, false, stream);
+}
+
+dc_status dc_halo_unpack(const dc_problem* prob, int32_t tile, int32_t which,
+                         const void* recv, void* t_pad, void* stream) {
+    return halo_common(prob, tile, which, recv, t_pad, true, stream);
+}
+
+dc_status dc_conv_fwd(const dc_problem* prob, int32_t tile, const void* x_pad,
+                      const void* w, float* y, void* stream) {
+    Geo g;
+    dc_status st = make_geo_tile(prob, tile, &g);
+    if (st != DC_OK) return st;
+    if (!x_pad || !w || !y) return DC_ERR_NULL;
+    if (misaligned(x_pad) || misaligned(w) || misaligned(y)) return DC_ERR_ALIGN;
+    IgemmArgs a;
+    igemm_common(g, tile, a);
+    a.in = x_pad; a.w = w; a.out = y;
+    a.in_tile = g.x_tile;
+    a.out_tile = int64_t(g.N) * g.K * g.Hot * g.Wot;
+    a.Cin = g.C; a.Cout = g.K;
+    a.in_rows = g.x_rows; a.in_cols = g.x_cols; a.in_pitch = g.x_pitch;
+    a.Uo = g.Hot; a.Vo = g.Wot;
+    a.out_rows = g.Hot; a.out_cols = g.Wot;
+    a.ostr = 1; a.oph_r = 0; a.oph_c = 0;
+    a.istr = g.stride;
+    a.Tr = g.R; a.Ts = g.S;
+    a.base_r = g.h - g.pad; a.base_c = g.h - g.pad;
+    a.wr0 = 0; a.wrstep = 1; a.ws0 = 0; a.wsstep = 1;
+    a.w_os = int64_t(g.C) * g.R * g.S; a.w_cs = int64_t(g.R) * g.S;
+    if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+    return launched(launch_igemm(a, g.dtype, static_cast<hipStream_t>(stream)));
+}
+
+dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_pad,
+                           const void* w, float* dx, void* stream) {
+    Geo g;
+    dc_status st = make_geo_tile(prob, tile, &g);
+    if (st != DC_OK) return st;
+    if (!dy_pad || !w || !dx) return DC_ERR_NULL;
+    if (misaligned(dy_pad) || misaligned(w) || misaligned(dx)) return DC_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int st_ = g.stride;
+    // Eq. (3) split by output phase (i mod stride, j mod stride): each phase
+    // is a stride-1 correlation of dy with the taps r = (phase+pad) mod stride
+    // + stride*t, visited in reverse.  At stride 1 there is one phase holding
+    // the whole filter reversed.
+    for (int phr = 0; phr < st_; ++phr) {
+        for (int phc = 0; phc < st_; ++phc) {
+            IgemmArgs a;
+            igemm_common(g, tile, a);
+            a.in = dy_pad; a.w = w; a.out = dx;
+            a.in_tile = g.dy_tile;
+            a.out_tile = int64_t(g.N) * g.C * g.Ht * g.Wt;
+            a.Cin = g.K; a.Cout = g.C;
+            a.in_rows = g.dy_rows; a.in_cols = g.dy_cols; a.in_pitch = g.dy_pitch;
+            a.out_rows = g.Ht; a.out_cols = g.Wt;
+            a.ostr = st_; a.oph_r = phr; a.oph_c = phc;
+            a.istr = 1;
+            const int rr = (phr + g.pad) % st_, rc = (phc + g.pad) % st_;
+            a.Tr = rr < g.R ? (g.R - rr + st_ - 1) / st_ : 0;
+            a.Ts = rc < g.S ? (g.S - rc + st_ - 1) / st_ : 0;
+            a.Uo = g.Ht > phr ? (g.Ht - phr + st_ - 1) / st_ : 0;
+            a.Vo = g.Wt > phc ? (g.Wt - phc + st_ - 1) / st_ : 0;
+            if (a.Uo == 0 || a.Vo == 0) continue;
+            a.base_r = g.h + (phr + g.pad - rr) / st_ - (a.Tr - 1);
+            a.base_c = g.h + (phc + g.pad - rc) / st_ - (a.Ts - 1);
+            a.wr0 = rr + st_ * (a.Tr - 1); a.wrstep = -st_;
+            a.ws0 = rc + st_ * (a.Ts - 1); a.wsstep = -st_;
+            if (a.Tr == 0 || a.Ts == 0) { a.Tr = 0; a.Ts = 0; a.base_r = 0; a.base_c = 0; }
+            a.w_os = int64_t(g.R) * g.S; a.w_cs = int64_t(g.C) * g.R * g.S;
+            if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+            dc_status r = launched(launch_igemm(a, g.dtype, s));
+            if (r != DC_OK) return r;
+        }
+    }
+    return DC_OK;
+}
+
+size_t dc_bwd_filter_workspace_bytes(const dc_problem* prob, int32_t tile) {
+    Geo g;
+    if (make_geo_tile(prob, tile, &g) != DC_OK) return 0;
+    int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
+    return wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.Hot, g.Wot);
+}
+
+dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x_pad,
+                             const void* dy_pad, float* dw, int32_t accumulate,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+    Geo g;
+    dc_status st = make_geo_tile(prob, tile, &g);
+    if (st != DC_OK) return st;
+    if (accumulate != 0 && accumulate != 1) return DC_ERR_ARG;
+    if (!x_pad || !dy_pad || !dw) return DC_ERR_NULL;
+    if (misaligned(x_pad) || misaligned(dy_pad) || misaligned(dw)) return DC_ERR_ALIGN;
+    const int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
+    size_t need = wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.Hot, g.Wot);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return DC_ERR_WORKSPACE;
+    if (need > 0 && misaligned(workspace)) return DC_ERR_ALIGN;
+    WgradArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.x = x_pad; a.dy = dy_pad; a.part = static_cast<float*>(workspace); a.dw = dw;
+    a.x_tile = g.x_tile; a.dy_tile = g.dy_tile;
+    a.ntiles = nt; a.Nn = g.N;
+    a.C = g.C; a.K = g.K; a.R = g.R; a.S = g.S;
+    a.x_rows = g.x_rows; a.x_cols = g.x_cols; a.x_pitch = g.x_pitch;
+    a.dy_pitch = g.dy_pitch; a.dy_off = g.h;
+    a.Hot = g.Hot; a.Wot = g.Wot;
+    a.istr = g.stride;
+    a.base_r = g.h - g.pad; a.base_c = g.h - g.pad;
+    a.accumulate = accumulate;
+    if (!wgrad_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+    return launched(launch_wgrad(a, g.dtype, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

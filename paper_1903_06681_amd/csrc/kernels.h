@@ -1,0 +1,109 @@
+// Launch interfaces of the HIP kernels behind the dc_* entry points.
+// Host code builds these argument blocks from a validated Geo; every kernel
+// trusts them (bounds were checked on the host).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dc {
+
+// ---------------------------------------------------------------- halo
+
+struct HaloRegion {
+    int rows, cols;      // region extent
+    int64_t off;         // element offset of the region in one packed buffer
+    int tr0, tc0;        // region origin in the padded tile (pack: source; unpack: margin)
+    int di, dj;          // direction of the neighbour
+    int opp;             // index of the opposite direction
+};
+
+struct HaloArgs {
+    const void* src;     // pack: padded tiles; unpack: packed buffers
+    void* dst;           // pack: packed buffers; unpack: padded tiles
+    int64_t tile_elems;  // elements per padded tile
+    int64_t halo_elems;  // elements per packed buffer
+    int planes;          // N * channels
+    int rows, pitch;     // padded tile rows and row pitch
+    int P, Q;
+    int tile0;           // first tile handled by this launch
+    int ntiles;          // tiles handled by this launch
+    int all_tiles;       // unpack: read neighbours' send buffers directly
+    HaloRegion reg[8];
+};
+
+hipError_t launch_halo_pack(const HaloArgs& a, int esize, hipStream_t s);
+hipError_t launch_halo_unpack(const HaloArgs& a, int esize, hipStream_t s);
+
+// ------------------------------------------- implicit-GEMM conv (fwd / bwd-data)
+//
+// out[n, o, u*ostr + oph_r, v*ostr + oph_c] =
+//     sum_{ci, tr, ts} in[n, ci, u*istr + tr + base_r, v*istr + ts + base_c]
+//                      * w[o*w_os + ci*w_cs + (wr0 + wrstep*tr)*S + (ws0 + wsstep*ts)]
+// for u < Uo, v < Vo.  Forward: in = x tile, o = filter.  Backward-data at
+// stride 1 (or one stride phase): in = dy tile, o = input channel, taps
+// reversed.  Input coordinates are padded-tile coordinates.
+
+struct IgemmArgs {
+    const void* in;
+    const void* w;
+    float* out;
+    int64_t in_tile, out_tile;   // elements between consecutive tiles (all-tiles mode)
+    int ntiles, Nn;
+    int Cin, Cout;
+    int in_rows, in_cols, in_pitch;
+    int Uo, Vo;
+    int out_rows, out_cols;
+    int ostr, oph_r, oph_c;
+    int istr;
+    int Tr, Ts;
+    int base_r, base_c;
+    int wr0, wrstep, ws0, wsstep;
+    int S;                       // filter width (weight index stride of r)
+    int64_t w_os, w_cs;          // weight strides of o and ci
+    int CC;                      // channels per LDS chunk (multiple of 8 for bf16, 2 for fp32)
+    int OB;                      // output channels per workgroup (32 or 64)
+    int lds_bytes;
+};
+
+// Largest dynamic LDS allocation per workgroup on the current device (bytes).
+int device_lds_limit();
+
+// Chooses the channel chunk and LDS size; returns false if no variant fits.
+bool igemm_plan(IgemmArgs& a, int dtype);
+hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s);
+
+// ----------------------------------------------------- weight gradient
+//
+// part[chunk][o][ci][r][s] = sum over the chunk's output pixels of
+//     dy[n, o, p, q] * x[n, ci, p*istr + r + base_r, q*istr + s + base_c]
+// then dw = (accumulate ? dw : 0) + sum_chunk part[chunk] in chunk order.
+
+struct WgradArgs {
+    const void* x;               // padded x tiles
+    const void* dy;              // padded dy tiles (interior read only)
+    float* part;                 // workspace partials [nchunks][K*C*R*S]
+    float* dw;
+    int64_t x_tile, dy_tile;
+    int ntiles, Nn;
+    int C, K, R, S;
+    int x_rows, x_cols, x_pitch;
+    int dy_pitch, dy_off;        // dy interior origin (= h) in the padded tile
+    int Hot, Wot;
+    int istr;
+    int base_r, base_c;
+    int chunks_per_tile;         // pixel-row chunks per tile
+    int rows_per_chunk;          // flattened (n, p) output rows per chunk
+    int nchunks;                 // ntiles * chunks_per_tile
+    int TRB;                     // filter rows handled per workgroup
+    int accumulate;
+    int lds_bytes;
+};
+
+size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
+                             int Hot, int Wot);
+bool wgrad_plan(WgradArgs& a, int dtype);
+hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s);
+
+}  // namespace dc

@@ -1,0 +1,165 @@
+"""Host-side checks of libdc that need no GPU: the library loads and exports
+every function include/dc.h declares, problems and arguments are validated
+before anything is launched, and the tile geometry agrees with the oracle's
+brute-force index sets (Sec. III-A)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle as orc
+import paper_1903_06681_amd as dc
+import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+# Fake device addresses for argument-checking tests.  Every call below is
+# invalid in exactly one respect that the library checks before any launch.
+A16, A32, A48, MIS = 0x10000, 0x20000, 0x30000, 0x10001
+
+
+def prob(**kw):
+    base = dict(N=2, C=8, K=8, H=32, W=32, R=3, S=3, stride=1, pad=1, P=2, Q=2, halo=1,
+                dtype=dc.DC_F32)
+    base.update(kw)
+    return dc.Problem(*[base[f] for f, _ in dc.Problem._fields_])
+
+
+def test_every_declared_function_is_exported():
+    hdr = open(os.path.join(ROOT, "include", "dc.h")).read()
+    names = set(re.findall(r"\b(dc_[a-z_]+)\s*\(", hdr))
+    assert {"dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter",
+            "dc_halo_pack", "dc_halo_unpack"} <= names
+    lib = dc.lib()
+    for n in sorted(names):
+        assert hasattr(lib, n), n
+    assert set(dc.EXPORTS) == names
+
+
+@pytest.mark.parametrize("kw,code", [
+    ({}, 0),
+    ({"N": 0}, -2), ({"C": -1}, -2), ({"R": 0}, -2), ({"stride": 0}, -2), ({"pad": -1}, -2),
+    ({"P": 0}, -2), ({"halo": -1}, -2),
+    ({"dtype": 7}, -3),
+    ({"halo": 0}, -4),                       # 3x3 needs 1
+    ({"R": 5, "S": 5, "pad": 2}, -4),        # needs 2, has 1
+    ({"halo": 17}, -4),                      # wider than a 16-wide tile
+    ({"H": 33}, -5),                         # uneven tiles
+    ({"stride": 2}, -5),                     # decomposed stride 2
+    ({"pad": 0, "halo": 2}, -5),             # decomposed, output not "same"
+    ({"H": 2, "W": 2, "P": 1, "Q": 1, "pad": 0}, -2),  # empty output
+    ({"P": 1, "Q": 1, "R": 1, "S": 1, "pad": 0, "halo": 0}, 0),
+    ({"P": 1, "Q": 1, "stride": 2}, 0),
+])
+def test_validate_status_codes(kw, code):
+    assert dc.validate(prob(**kw), dc.DC_ALL_TILES) == code
+
+
+def test_tile_index_range():
+    p = prob()
+    assert dc.validate(p, 3) == 0
+    assert dc.validate(p, 4) == -9
+    assert dc.validate(p, -2) == -9
+
+
+def test_all_workloads_validate():
+    for L in wl.LAYERS.values():
+        p = dc.Problem.of(L)
+        assert dc.validate(p, dc.DC_ALL_TILES) == 0, L.name
+        assert dc.tile_dims(p) == (L.Ht, L.Wt, L.Hot, L.Wot)
+
+
+@pytest.mark.parametrize("R,stride,pad,H,P", [
+    (3, 1, 1, 32, 2), (5, 1, 2, 40, 4), (1, 1, 0, 16, 2), (7, 2, 3, 224, 1), (3, 2, 1, 16, 1),
+    (3, 1, 0, 12, 1), (4, 1, 1, 20, 1), (1, 2, 0, 14, 1), (5, 2, 1, 21, 1), (3, 3, 2, 17, 1),
+])
+def test_required_halo_matches_brute_force(R, stride, pad, H, P):
+    p = prob(R=R, S=R, stride=stride, pad=pad, H=H, W=H, P=P, Q=P, halo=max(R, 3))
+    lohi_x = dc.required_halo(p, dc.DC_X)
+    lohi_dy = dc.required_halo(p, dc.DC_DY)
+    Ho = orc.out_size(H, R, stride, pad)
+    Ht, Hot = H // P, Ho // P
+    bx = [0, 0]
+    bd = [0, 0]
+    for ti in range(P):
+        lo, hi = orc.needed_halo_x(H, R, stride, pad, Ho, Ht, Hot, ti * Hot, ti * Ht)
+        bx = [max(bx[0], lo), max(bx[1], hi)]
+        lo, hi = orc.needed_halo_dy(Ho, R, stride, pad, Ht, Hot, ti * Ht, ti * Hot)
+        bd = [max(bd[0], lo), max(bd[1], hi)]
+    assert list(lohi_x) == bx
+    assert list(lohi_dy) == bd
+
+
+def test_one_by_one_needs_no_halo_and_packs_nothing():
+    p = prob(R=1, S=1, pad=0, halo=0)
+    assert dc.required_halo(p, dc.DC_X) == (0, 0)
+    assert dc.halo_elems(p, dc.DC_X) == 0
+    # h = 0: pack/unpack are no-ops that succeed without touching memory
+    dc.halo_pack(p, dc.DC_ALL_TILES, dc.DC_X, A16, A32, 0)
+    dc.halo_unpack(p, dc.DC_ALL_TILES, dc.DC_X, A16, A32, 0)
+
+
+def test_halo_elems_and_pitch_match_oracle_layout():
+    for L in wl.LAYERS.values():
+        p = dc.Problem.of(L)
+        for which, ch, th, tw in ((dc.DC_X, L.C, L.Ht, L.Wt), (dc.DC_DY, L.K, L.Hot, L.Wot)):
+            _, total = orc.region_offsets(L.N, ch, th, tw, L.halo)
+            assert dc.halo_elems(p, which) == total
+            pitch = dc.tile_pitch(p, which)
+            esize = 2 if L.dtype == "bf16" else 4
+            assert pitch >= tw + 2 * L.halo and (pitch * esize) % 16 == 0
+            assert dc.tile_elems(p, which) == L.N * ch * (th + 2 * L.halo) * pitch
+
+
+def _status(fn, *args):
+    with pytest.raises(dc.DcError) as e:
+        fn(*args)
+    return e.value.status
+
+
+def test_calls_reject_bad_arguments_before_launch():
+    p = prob()
+    bad = prob(H=33)
+    assert _status(dc.conv_fwd, bad, 0, A16, A32, A48, 0) == -5
+    assert _status(dc.conv_fwd, p, 4, A16, A32, A48, 0) == -9
+    assert _status(dc.conv_fwd, p, 0, None, A32, A48, 0) == -1
+    assert _status(dc.conv_fwd, p, 0, MIS, A32, A48, 0) == -7
+    assert _status(dc.conv_bwd_data, p, 0, A16, None, A48, 0) == -1
+    assert _status(dc.conv_bwd_data, p, 0, A16, A32, MIS, 0) == -7
+    assert _status(dc.halo_pack, p, 0, 2, A16, A32, 0) == -10
+    assert _status(dc.halo_unpack, p, 0, dc.DC_X, None, A32, 0) == -1
+    assert _status(dc.halo_unpack, p, 0, dc.DC_DY, A16, MIS, 0) == -7
+
+
+class _FakeWs:
+    def __init__(self, ptr, nbytes):
+        self.ptr, self.nbytes = ptr, nbytes
+
+    def numel(self):
+        return self.nbytes
+
+    def element_size(self):
+        return 1
+
+    def data_ptr(self):
+        return self.ptr
+
+
+def test_bwd_filter_workspace_and_flags_checked():
+    p = prob()
+    need = dc.bwd_filter_workspace_bytes(p, 0)
+    assert need > 0
+    assert dc.bwd_filter_workspace_bytes(p, dc.DC_ALL_TILES) >= need
+    assert _status(dc.conv_bwd_filter, p, 0, A16, A32, A48, 2, _FakeWs(A16, need), 0) == -10
+    assert _status(dc.conv_bwd_filter, p, 0, A16, A32, A48, 0, None, 0) == -6
+    assert _status(dc.conv_bwd_filter, p, 0, A16, A32, A48, 0, _FakeWs(A16, need - 4), 0) == -6
+    assert _status(dc.conv_bwd_filter, p, 0, A16, A32, A48, 0, _FakeWs(MIS, need), 0) == -7
+    assert _status(dc.conv_bwd_filter, p, 0, A16, None, A48, 0, _FakeWs(A16, need), 0) == -1
+
+
+def test_status_strings():
+    for code, name in dc.STATUS.items():
+        s = dc.lib().dc_status_string(code)
+        assert isinstance(s, bytes) and len(s) > 0
+    assert dc.lib().dc_status_string(-99) == b"unknown status"
