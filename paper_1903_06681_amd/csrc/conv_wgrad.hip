@@ -4,24 +4,31 @@
 //   dw[o][ci, r, s] = sum_{pixels} dy[o][pixel] * x[ci][pixel shifted by (r, s)]
 //
 // NCHW keeps both operands contiguous along the reduction (pixels), so no
-// transpose is needed.  The pixel range of a tile is split into chunks of
-// output rows; each workgroup reduces one chunk into a partial dw slice in
-// the workspace, and a second kernel adds the partials in chunk order (fixed
-// order, no atomics: deterministic).  Only the interior of the dy tile is
-// read -- the weight gradient needs no dy halo (Sec. III-A).
+// transpose is needed.  The pixels of a tile are split into chunks; each
+// workgroup reduces one chunk into a partial in the workspace, and a second
+// kernel adds the partials in chunk order (fixed order, no atomics:
+// deterministic).  Only the interior of the dy tile is read -- the weight
+// gradient needs no dy halo (Sec. III-A).
 //
-// bf16: v_mfma_f32_32x32x16_bf16, a k-step of 16 pixels (8 per half-wave).
-//       Four waves = 2 blocks of 32 filters x 2 blocks of 32 channels; each
-//       wave accumulates its 32 x 32 block at every tap (r, s) of its filter
-//       rows.  The 8 pixels a lane feeds for tap s start s elements into the
-//       staged x row: two aligned 16-byte LDS reads give a 16-element window
-//       from which every shift is cut with byte-align operations.
-// fp32: v_mfma_f32_32x32x2_f32, a k-step of 2 pixels (one per half-wave);
-//       columns are the flattened (ci, r, s) index in blocks of 32, and each
-//       lane reads its own single x value.
+// Strip kernel (bf16, stride 1): a workgroup walks down a 64-column strip of
+// one sample.  x rows live in an LDS ring (a new row per output row, the
+// filter rows reuse the previous ones) next to a double-buffered dy row; the
+// next row's 16-byte global loads are in flight while the current row runs
+// on v_mfma_f32_32x32x16_bf16.  Four waves = 2 blocks of 32 filters x 2
+// blocks of 32 channels; each wave keeps its 32 x 32 block at every tap of
+// its filter rows in accumulators.  A k-step is 16 pixels (8 per half-wave);
+// the 8 pixels a lane feeds for tap s start s elements into the staged x row,
+// cut from two aligned 16-byte LDS reads with byte-align operations.
+// Partials are stored in MFMA fragment order (coalesced) and mapped back to
+// the dw layout by the reduction.
+//
+// Row kernels (general fallback: bf16 stride > 1, fp32): stage one output row
+// segment per step; partials in dw order.  fp32 uses v_mfma_f32_32x32x2_f32
+// with flattened (ci, r, s) columns in blocks of 32.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstring>
 
 #include "kernels.h"
 
@@ -43,42 +50,7 @@ union Pack8 {
 
 // ---------------------------------------------------------------- planning
 
-struct WgradGrid {
-    int gy, gz;               // tap-row groups / column groups, filter/channel superblocks
-    int chunks_per_tile, rows_per_chunk;
-    int TRB;                  // bf16: filter rows per workgroup
-};
-
 static int bf16_trb(int S) { return std::max(1, 9 / S); }
-
-static bool wgrad_grid(int dtype, int ntiles, int N, int C, int K, int R, int S, int Hot,
-                       WgradGrid* g) {
-    if (dtype == 1) {
-        if (S > 7) return false;
-        g->TRB = std::min(bf16_trb(S), R);
-        g->gy = (R + g->TRB - 1) / g->TRB;
-        g->gz = ((K + 63) / 64) * ((C + 63) / 64);
-    } else {
-        const int NCB = (C * R * S + 31) / 32;
-        g->TRB = R;
-        g->gy = (NCB + 7) / 8;   // 4 waves x 2 column blocks per workgroup
-        g->gz = (K + 63) / 64;
-    }
-    const int rows = N * Hot;
-    int want = std::max(1, kTargetWGs / (g->gy * g->gz));
-    int cpt = std::max(1, std::min(rows, (want + ntiles - 1) / ntiles));
-    g->rows_per_chunk = (rows + cpt - 1) / cpt;
-    g->chunks_per_tile = (rows + g->rows_per_chunk - 1) / g->rows_per_chunk;
-    return true;
-}
-
-size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
-                             int Hot, int Wot) {
-    (void)Wot;
-    WgradGrid g;
-    if (!wgrad_grid(dtype, ntiles, N, C, K, R, S, Hot, &g)) return 0;
-    return size_t(ntiles) * g.chunks_per_tile * size_t(K) * C * R * S * sizeof(float);
-}
 
 __host__ __device__ inline int bf16_xwp(int istr, int S) {
     int xw = (kBQ - 1) * istr + S;
@@ -92,15 +64,79 @@ __host__ __device__ inline int odd16(int elems) {
     return u * 8;
 }
 static constexpr int kDyP = 72;   // staged dy row pitch (bf16): 9 x 16 bytes
+static constexpr int kXP = 72;    // strip kernel: staged x row pitch (bf16): 9 x 16 bytes
+
+struct Plan {
+    int kind, gy, gz, TRB, nchunks;
+    int chunks_per_tile, rows_per_chunk;
+    int nqb, nseg, rows_per_seg;
+    int64_t F;
+    int frag;
+};
+
+static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, int stride,
+                      int Hot, int Wot, Plan* pl) {
+    std::memset(pl, 0, sizeof(*pl));
+    if (dtype == 1 && stride == 1 && S <= 7) {
+        pl->kind = WGRAD_STRIP_BF16;
+        pl->TRB = std::min(bf16_trb(S), R);
+        pl->gy = (R + pl->TRB - 1) / pl->TRB;
+        pl->gz = ((K + 63) / 64) * ((C + 63) / 64);
+        pl->nqb = (Wot + kBQ - 1) / kBQ;
+        const int strips = ntiles * N * pl->nqb;
+        const int want = std::max(1, kTargetWGs / (pl->gy * pl->gz));
+        int nseg = std::max(1, std::min(Hot, (want + strips - 1) / strips));
+        pl->rows_per_seg = (Hot + nseg - 1) / nseg;
+        pl->nseg = (Hot + pl->rows_per_seg - 1) / pl->rows_per_seg;
+        pl->nchunks = strips * pl->nseg;
+        // template capacity: filter rows x S taps per wave
+        const int trb_cap = S == 1 ? 9 : std::max(1, 9 / S);
+        pl->F = int64_t(pl->gy) * pl->gz * 4 * trb_cap * S * 1024;
+        pl->frag = 1;
+        return true;
+    }
+    if (dtype == 1) {
+        if (S > 7) return false;
+        pl->kind = WGRAD_ROWS_BF16;
+        pl->TRB = std::min(bf16_trb(S), R);
+        pl->gy = (R + pl->TRB - 1) / pl->TRB;
+        pl->gz = ((K + 63) / 64) * ((C + 63) / 64);
+    } else {
+        const int NCB = (C * R * S + 31) / 32;
+        pl->kind = WGRAD_ROWS_F32;
+        pl->TRB = R;
+        pl->gy = (NCB + 7) / 8;   // 4 waves x 2 column blocks per workgroup
+        pl->gz = (K + 63) / 64;
+    }
+    const int rows = N * Hot;
+    const int want = std::max(1, kTargetWGs / (pl->gy * pl->gz));
+    const int cpt = std::max(1, std::min(rows, (want + ntiles - 1) / ntiles));
+    pl->rows_per_chunk = (rows + cpt - 1) / cpt;
+    pl->chunks_per_tile = (rows + pl->rows_per_chunk - 1) / pl->rows_per_chunk;
+    pl->nchunks = ntiles * pl->chunks_per_tile;
+    pl->F = int64_t(K) * C * R * S;
+    pl->frag = 0;
+    return true;
+}
+
+size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
+                             int stride, int Hot, int Wot) {
+    Plan pl;
+    if (!make_plan(dtype, ntiles, N, C, K, R, S, stride, Hot, Wot, &pl)) return 0;
+    return size_t(pl.nchunks) * size_t(pl.F) * sizeof(float);
+}
 
 bool wgrad_plan(WgradArgs& a, int dtype) {
-    WgradGrid g;
-    if (!wgrad_grid(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.Hot, &g)) return false;
-    a.TRB = g.TRB;
-    a.chunks_per_tile = g.chunks_per_tile;
-    a.rows_per_chunk = g.rows_per_chunk;
-    a.nchunks = a.ntiles * g.chunks_per_tile;
-    if (dtype == 1) {
+    Plan pl;
+    if (!make_plan(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.istr, a.Hot, a.Wot, &pl))
+        return false;
+    a.kind = pl.kind; a.gy = pl.gy; a.gz = pl.gz; a.TRB = pl.TRB; a.nchunks = pl.nchunks;
+    a.chunks_per_tile = pl.chunks_per_tile; a.rows_per_chunk = pl.rows_per_chunk;
+    a.nqb = pl.nqb; a.nseg = pl.nseg; a.rows_per_seg = pl.rows_per_seg;
+    a.F = pl.F; a.frag = pl.frag;
+    if (a.kind == WGRAD_STRIP_BF16) {
+        a.lds_bytes = ((a.TRB + 1) * 64 * kXP + 2 * 64 * kXP) * 2;
+    } else if (a.kind == WGRAD_ROWS_BF16) {
         const int plane = odd16(a.TRB * bf16_xwp(a.istr, a.S));
         a.lds_bytes = (64 * kDyP + 64 * plane) * 2;
     } else {
@@ -112,10 +148,227 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
     return a.lds_bytes <= device_lds_limit();
 }
 
+// ---------------------------------------------------------------- strip kernel (bf16)
+
+// Elements [sh, sh+8) of the 16-element window d[0..7] (two aligned 16-byte chunks).
+template <int SH>
+__device__ __forceinline__ uint4 window8(const uint32_t (&d)[8]) {
+    uint4 r;
+    uint32_t* o = reinterpret_cast<uint32_t*>(&r);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if ((SH & 1) == 0)
+            o[i] = d[SH / 2 + i];
+        else
+            o[i] = __builtin_amdgcn_alignbyte(d[SH / 2 + i + 1], d[SH / 2 + i], 2);
+    }
+    return r;
+}
+
+__device__ __forceinline__ uint4 window8_rt(const uint32_t (&d)[8], int sh) {
+    switch (sh) {
+        case 0: return window8<0>(d);
+        case 1: return window8<1>(d);
+        case 2: return window8<2>(d);
+        case 3: return window8<3>(d);
+        case 4: return window8<4>(d);
+        case 5: return window8<5>(d);
+        case 6: return window8<6>(d);
+        default: return window8<7>(d);
+    }
+}
+
+// 8 consecutive bf16 of a row starting at column g (any alignment); zero for
+// columns outside [0, ncols).  row is 16-byte aligned and has `pitch` (a
+// multiple of 8) readable elements.
+__device__ __forceinline__ uint4 load_row8(const uint16_t* row, int g, int ncols, int pitch,
+                                           bool row_ok) {
+    uint4 z = make_uint4(0, 0, 0, 0);
+    if (!row_ok || g >= ncols) return z;
+    const int ga = g & ~7, sh = g - ga;
+    uint4 v0 = (ga < pitch) ? *reinterpret_cast<const uint4*>(row + ga) : z;
+    uint4 v;
+    if (sh == 0) {
+        v = v0;
+    } else {
+        uint4 v1 = (ga + 8 < pitch) ? *reinterpret_cast<const uint4*>(row + ga + 8) : z;
+        const uint32_t d[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        v = window8_rt(d, sh);
+    }
+    const int nv = ncols - g;   // valid elements in this group of 8
+    if (nv < 8) {
+        uint32_t* w = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint32_t m = (2 * i < nv ? 0x0000ffffu : 0u) | (2 * i + 1 < nv ? 0xffff0000u : 0u);
+            w[i] &= m;
+        }
+    }
+    return v;
+}
+
+template <int SS, int TRB>
+__global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int NR = a.TRB + 1;                               // x ring slots
+    uint16_t* xring = reinterpret_cast<uint16_t*>(smem);    // [NR][64 ci][kXP]
+    uint16_t* dyb = xring + NR * 64 * kXP;                  // [2][64 o][kXP]
+
+    int c = blockIdx.x;
+    const int seg = c % a.nseg; c /= a.nseg;
+    const int qb = c % a.nqb; c /= a.nqb;
+    const int n = c % a.Nn;
+    const int tile = c / a.Nn;
+    const int p0 = seg * a.rows_per_seg;
+    const int nrows = min(a.rows_per_seg, a.Hot - p0);
+    const int q0 = qb * kBQ;
+    const int r0 = blockIdx.y * a.TRB;
+    const int nTR = min(a.TRB, a.R - r0);
+    const int ncsb = (a.C + 63) / 64;
+    const int o0 = (blockIdx.z / ncsb) * 64, c0 = (blockIdx.z % ncsb) * 64;
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int ow = wave & 1, cw = wave >> 1;
+
+    const uint16_t* xt = static_cast<const uint16_t*>(a.x) + tile * a.x_tile +
+                         int64_t(n) * a.C * a.x_rows * a.x_pitch;
+    const int dy_rows = a.Hot + 2 * a.dy_off;
+    const uint16_t* dyt = static_cast<const uint16_t*>(a.dy) + tile * a.dy_tile +
+                          int64_t(n) * a.K * dy_rows * a.dy_pitch;
+    const int64_t xplane = int64_t(a.x_rows) * a.x_pitch;
+    const int64_t dyplane = int64_t(dy_rows) * a.dy_pitch;
+    const int xg0 = q0 + a.base_c;                 // global column of staged x column 0
+    const int dyg0 = q0 + a.dy_off;                // global column of staged dy column 0
+    const int dy_end = a.dy_off + a.Wot;           // dy interior ends here
+    const int xrow0 = p0 + a.base_r + r0;          // x row of ring row 0
+
+    // staging units: x row = 64 channels x 9 groups of 8; dy row = 64 filters x 8 groups
+    constexpr int XU = 64 * 9, DU = 64 * 8;
+    constexpr int XPT = (XU + kThreads - 1) / kThreads, DPT = DU / kThreads;
+    uint4 xv[XPT], dv[DPT];
+
+    auto load_x = [&](int m) {   // ring row m -> registers
+        const int gr = xrow0 + m;
+        const bool rok = gr >= 0 && gr < a.x_rows;
+#pragma unroll
+        for (int k = 0; k < XPT; ++k) {
+            const int u = tid + k * kThreads;
+            xv[k] = make_uint4(0, 0, 0, 0);
+            if (u < XU) {
+                const int ci = u / 9, g8 = u - ci * 9;
+                if (c0 + ci < a.C)
+                    xv[k] = load_row8(xt + (c0 + ci) * xplane + int64_t(gr) * a.x_pitch,
+                                      xg0 + 8 * g8, a.x_cols, a.x_pitch, rok);
+            }
+        }
+    };
+    auto store_x = [&](int m) {
+        uint16_t* slot = xring + (m % NR) * 64 * kXP;
+#pragma unroll
+        for (int k = 0; k < XPT; ++k) {
+            const int u = tid + k * kThreads;
+            if (u < XU) {
+                const int ci = u / 9, g8 = u - ci * 9;
+                *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = xv[k];
+            }
+        }
+    };
+    auto load_dy = [&](int i) {   // output row p0 + i -> registers
+        const int gr = p0 + i + a.dy_off;
+#pragma unroll
+        for (int k = 0; k < DPT; ++k) {
+            const int u = tid + k * kThreads;
+            const int o = u >> 3, g8 = u & 7;
+            dv[k] = make_uint4(0, 0, 0, 0);
+            if (o0 + o < a.K)
+                dv[k] = load_row8(dyt + (o0 + o) * dyplane + int64_t(gr) * a.dy_pitch,
+                                  dyg0 + 8 * g8, dy_end, a.dy_pitch, true);
+        }
+    };
+    auto store_dy = [&](int i) {
+        uint16_t* slot = dyb + (i & 1) * 64 * kXP;
+#pragma unroll
+        for (int k = 0; k < DPT; ++k) {
+            const int u = tid + k * kThreads;
+            const int o = u >> 3, g8 = u & 7;
+            *reinterpret_cast<uint4*>(slot + o * kXP + 8 * g8) = dv[k];
+        }
+    };
+
+    floatx16 acc[TRB][SS];
+#pragma unroll
+    for (int i = 0; i < TRB; ++i)
+#pragma unroll
+        for (int j = 0; j < SS; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    // prologue: the filter rows of the first output row, and its dy row
+    for (int m = 0; m < nTR; ++m) {
+        load_x(m);
+        store_x(m);
+    }
+    load_dy(0);
+    store_dy(0);
+    __syncthreads();
+
+    const int qmax = min(kBQ, a.Wot - q0);
+    for (int i = 0; i < nrows; ++i) {
+        const bool more = i + 1 < nrows;
+        if (more) {           // next row's data in flight during this row's MFMAs
+            load_x(i + nTR);
+            load_dy(i + 1);
+        }
+        const uint16_t* dyrow = dyb + (i & 1) * 64 * kXP + (ow * 32 + l32) * kXP;
+        for (int kq = 0; kq < qmax; kq += 16) {
+            const int qc = kq + 8 * hi;
+            Pack8 A;
+            A.v = *reinterpret_cast<const uint4*>(dyrow + qc);
+#pragma unroll
+            for (int tr = 0; tr < TRB; ++tr) {
+                if (tr >= nTR) continue;
+                const uint16_t* xr = xring + ((i + tr) % NR) * 64 * kXP + (cw * 32 + l32) * kXP;
+                Pack8 lo, hh;
+                lo.v = *reinterpret_cast<const uint4*>(xr + qc);
+                hh.v = *reinterpret_cast<const uint4*>(xr + qc + 8);
+                const uint32_t d[8] = {lo.d[0], lo.d[1], lo.d[2], lo.d[3],
+                                       hh.d[0], hh.d[1], hh.d[2], hh.d[3]};
+#pragma unroll
+                for (int s = 0; s < SS; ++s) {
+                    Pack8 B;
+                    B.v = (s == 0) ? window8<0>(d) : (s == 1) ? window8<1>(d) : (s == 2) ? window8<2>(d)
+                        : (s == 3) ? window8<3>(d) : (s == 4) ? window8<4>(d) : (s == 5) ? window8<5>(d)
+                        : window8<6>(d);
+                    acc[tr][s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.b, B.b, acc[tr][s], 0, 0, 0);
+                }
+            }
+        }
+        if (more) {
+            store_x(i + nTR);
+            store_dy(i + 1);
+        }
+        __syncthreads();
+    }
+
+    // partial in fragment order: [chunk][gy][gz][wave][tr][s][16][64]
+    float* part = a.part + int64_t(blockIdx.x) * a.F +
+                  ((int64_t(blockIdx.y) * a.gz + blockIdx.z) * 4 + wave) * TRB * SS * 1024;
+#pragma unroll
+    for (int tr = 0; tr < TRB; ++tr) {
+        if (tr >= nTR) continue;
+#pragma unroll
+        for (int s = 0; s < SS; ++s)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                part[(tr * SS + s) * 1024 + e * 64 + lane] = acc[tr][s][e];
+    }
+}
+
 // ---------------------------------------------------------------- bf16
 
 template <int SS, int TRB>
-__global__ __launch_bounds__(kThreads) void wgrad_bf16_kernel(WgradArgs a) {
+__global__ __launch_bounds__(kThreads) void wgrad_rows_bf16_kernel(WgradArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int XWP = bf16_xwp(a.istr, SS);
     const int PLANE = odd16(a.TRB * XWP);   // a.TRB <= TRB rows are staged
@@ -224,7 +477,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_kernel(WgradArgs a) {
     }
 
     // partial slice: rows = filters, columns = channels (D layout of the 32x32 tile)
-    float* part = a.part + int64_t(chunk) * a.K * a.C * a.R * a.S;
+    float* part = a.part + int64_t(chunk) * a.F;
     const int ci = c0 + cw * 32 + l32;
     if (ci >= a.C) return;
 #pragma unroll
@@ -244,7 +497,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_bf16_kernel(WgradArgs a) {
 // ---------------------------------------------------------------- fp32
 
 template <int NBW>
-__global__ __launch_bounds__(kThreads) void wgrad_f32_kernel(WgradArgs a) {
+__global__ __launch_bounds__(kThreads) void wgrad_rows_f32_kernel(WgradArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int DYP = kBQ + 1;
     float* dyl = reinterpret_cast<float*>(smem);   // [64 o][DYP]
@@ -346,7 +599,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_kernel(WgradArgs a) {
     }
 
     if (!wave_active) return;
-    float* part = a.part + int64_t(chunk) * a.K * CRS;
+    float* part = a.part + int64_t(chunk) * a.F;
 #pragma unroll
     for (int ob = 0; ob < 2; ++ob) {
         if (ob >= NOB) continue;
@@ -365,15 +618,46 @@ __global__ __launch_bounds__(kThreads) void wgrad_f32_kernel(WgradArgs a) {
 
 // ---------------------------------------------------------------- reduction
 
-// dw[e] = (accumulate ? dw[e] : 0) + sum_{c = 0..nchunks-1} part[c][e], in chunk order.
-__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ part,
-                                                           float* __restrict__ dw, int64_t E,
-                                                           int nchunks, int accumulate) {
-    const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
-    if (e >= E) return;
-    float s = 0.f;
-    for (int c = 0; c < nchunks; ++c) s += part[int64_t(c) * E + e];
-    dw[e] = accumulate ? dw[e] + s : s;
+// dw = (accumulate ? dw : 0) + sum over chunks of the partials, in a fixed
+// order: chunk group g (of 4) sums chunks g, g+4, g+8, ... in increasing
+// order, then the four group sums are added in order 0..3.  A workgroup
+// covers 64 partial positions x 4 chunk groups; loads are coalesced along
+// the positions.
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
+    __shared__ float red[4][64];
+    const int64_t f = int64_t(blockIdx.x) * 64 + (threadIdx.x & 63);
+    const int g = threadIdx.x >> 6;
+    float sum = 0.f;
+    if (f < a.F)
+        for (int c = g; c < a.nchunks; c += 4) sum += a.part[int64_t(c) * a.F + f];
+    red[g][threadIdx.x & 63] = sum;
+    __syncthreads();
+    if (g != 0 || f >= a.F) return;
+    const int l = threadIdx.x;
+    const float total = ((red[0][l] + red[1][l]) + red[2][l]) + red[3][l];
+    int64_t idx;
+    if (a.frag) {
+        // [gy][gz][wave][tr][s][16][64] -> (o, ci, r, s)
+        const int SS = a.S;
+        const int trb_cap = a.S == 1 ? 9 : max(1, 9 / a.S);
+        int64_t t = f;
+        const int lane = int(t % 64); t /= 64;
+        const int e = int(t % 16); t /= 16;
+        const int s = int(t % SS); t /= SS;
+        const int tr = int(t % trb_cap); t /= trb_cap;
+        const int wave = int(t % 4); t /= 4;
+        const int bz = int(t % a.gz);
+        const int by = int(t / a.gz);
+        const int ncsb = (a.C + 63) / 64;
+        const int o = (bz / ncsb) * 64 + (wave & 1) * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
+        const int ci = (bz % ncsb) * 64 + (wave >> 1) * 32 + (lane & 31);
+        const int r = by * a.TRB + tr;
+        if (tr >= a.TRB || r >= a.R || o >= a.K || ci >= a.C) return;
+        idx = ((int64_t(o) * a.C + ci) * a.R + r) * a.S + s;
+    } else {
+        idx = f;
+    }
+    a.dw[idx] = a.accumulate ? a.dw[idx] + total : total;
 }
 
 template <typename K>
@@ -383,41 +667,57 @@ static hipError_t set_lds(K kernel, int bytes) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
-template <int SS>
-static hipError_t launch_bf16(const WgradArgs& a, dim3 grid, hipStream_t s) {
-    constexpr int TRB = SS == 1 ? 9 : (9 / SS > 0 ? 9 / SS : 1);
-    hipError_t e = set_lds(wgrad_bf16_kernel<SS, TRB>, a.lds_bytes);
+template <int SS, int TRB>
+static hipError_t launch_strip(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    hipError_t e = set_lds(wgrad_strip_bf16_kernel<SS, TRB>, a.lds_bytes);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((wgrad_bf16_kernel<SS, TRB>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    hipLaunchKernelGGL((wgrad_strip_bf16_kernel<SS, TRB>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
+template <int SS>
+static hipError_t launch_rows_bf16(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    constexpr int TRB = SS == 1 ? 9 : (9 / SS > 0 ? 9 / SS : 1);
+    hipError_t e = set_lds(wgrad_rows_bf16_kernel<SS, TRB>, a.lds_bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((wgrad_rows_bf16_kernel<SS, TRB>), grid, dim3(kThreads), a.lds_bytes, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
-    WgradGrid g;
-    wgrad_grid(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.Hot, &g);
-    dim3 grid(a.nchunks, g.gy, g.gz);
-    hipError_t e = hipSuccess;
-    if (dtype == 1) {
+    dim3 grid(a.nchunks, a.gy, a.gz);
+    hipError_t e = hipErrorInvalidValue;
+    if (a.kind == WGRAD_STRIP_BF16) {
+        // the accumulator capacity (TRB rows x S taps) is fixed per filter width
         switch (a.S) {
-            case 1: e = launch_bf16<1>(a, grid, s); break;
-            case 2: e = launch_bf16<2>(a, grid, s); break;
-            case 3: e = launch_bf16<3>(a, grid, s); break;
-            case 4: e = launch_bf16<4>(a, grid, s); break;
-            case 5: e = launch_bf16<5>(a, grid, s); break;
-            case 6: e = launch_bf16<6>(a, grid, s); break;
-            case 7: e = launch_bf16<7>(a, grid, s); break;
+            case 1: e = launch_strip<1, 9>(a, grid, s); break;
+            case 2: e = launch_strip<2, 4>(a, grid, s); break;
+            case 3: e = launch_strip<3, 3>(a, grid, s); break;
+            case 4: e = launch_strip<4, 2>(a, grid, s); break;
+            case 5: e = launch_strip<5, 1>(a, grid, s); break;
+            case 6: e = launch_strip<6, 1>(a, grid, s); break;
+            case 7: e = launch_strip<7, 1>(a, grid, s); break;
+            default: return hipErrorInvalidValue;
+        }
+    } else if (a.kind == WGRAD_ROWS_BF16) {
+        switch (a.S) {
+            case 1: e = launch_rows_bf16<1>(a, grid, s); break;
+            case 2: e = launch_rows_bf16<2>(a, grid, s); break;
+            case 3: e = launch_rows_bf16<3>(a, grid, s); break;
+            case 4: e = launch_rows_bf16<4>(a, grid, s); break;
+            case 5: e = launch_rows_bf16<5>(a, grid, s); break;
+            case 6: e = launch_rows_bf16<6>(a, grid, s); break;
+            case 7: e = launch_rows_bf16<7>(a, grid, s); break;
             default: return hipErrorInvalidValue;
         }
     } else {
-        e = set_lds(wgrad_f32_kernel<2>, a.lds_bytes);
+        e = set_lds(wgrad_rows_f32_kernel<2>, a.lds_bytes);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(wgrad_f32_kernel<2>, grid, dim3(kThreads), a.lds_bytes, s, a);
+        hipLaunchKernelGGL(wgrad_rows_f32_kernel<2>, grid, dim3(kThreads), a.lds_bytes, s, a);
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;
-    const int64_t E = int64_t(a.K) * a.C * a.R * a.S;
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(unsigned((E + 255) / 256)), dim3(256), 0, s,
-                       a.part, a.dw, E, a.nchunks, a.accumulate);
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(unsigned((a.F + 63) / 64)), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -76,14 +76,18 @@ hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s);
 
 // ----------------------------------------------------- weight gradient
 //
-// part[chunk][o][ci][r][s] = sum over the chunk's output pixels of
-//     dy[n, o, p, q] * x[n, ci, p*istr + r + base_r, q*istr + s + base_c]
-// then dw = (accumulate ? dw : 0) + sum_chunk part[chunk] in chunk order.
+// Each workgroup reduces one chunk of a tile's output pixels into a partial
+// weight gradient in the workspace; a second kernel adds the partials in
+// chunk order:  dw = (accumulate ? dw : 0) + sum_chunk part[chunk].
+//   part = dy[n, o, p, q] * x[n, ci, p*istr + r + base_r, q*istr + s + base_c]
+// summed over the chunk's (n, p, q).
+
+enum WgradKind { WGRAD_STRIP_BF16 = 0, WGRAD_ROWS_BF16 = 1, WGRAD_ROWS_F32 = 2 };
 
 struct WgradArgs {
     const void* x;               // padded x tiles
     const void* dy;              // padded dy tiles (interior read only)
-    float* part;                 // workspace partials [nchunks][K*C*R*S]
+    float* part;                 // workspace partials [nchunks][F]
     float* dw;
     int64_t x_tile, dy_tile;
     int ntiles, Nn;
@@ -93,16 +97,21 @@ struct WgradArgs {
     int Hot, Wot;
     int istr;
     int base_r, base_c;
-    int chunks_per_tile;         // pixel-row chunks per tile
-    int rows_per_chunk;          // flattened (n, p) output rows per chunk
-    int nchunks;                 // ntiles * chunks_per_tile
-    int TRB;                     // filter rows handled per workgroup
     int accumulate;
+    // plan
+    int kind;                    // WgradKind
+    int gy, gz;                  // grid: filter-row groups (or column groups), channel superblocks
+    int TRB;                     // filter rows per workgroup
+    int nchunks;
+    int chunks_per_tile, rows_per_chunk;   // row kinds: flattened (n, p) rows per chunk
+    int nqb, nseg, rows_per_seg;           // strip kind: 64-column strips, row segments
+    int64_t F;                   // floats per chunk partial
+    int frag;                    // 1: partials in MFMA fragment order, 0: in dw order
     int lds_bytes;
 };
 
 size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
-                             int Hot, int Wot);
+                             int stride, int Hot, int Wot);
 bool wgrad_plan(WgradArgs& a, int dtype);
 hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s);
 
