@@ -23,12 +23,11 @@
 
 #include <algorithm>
 
+#include "bf16util.h"
 #include "kernels.h"
 
 namespace dc {
 
-typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 
 static constexpr int kThreads = 256;
 static constexpr int kBH = 4;    // output rows per workgroup (one per wave)
@@ -47,10 +46,6 @@ __host__ __device__ inline int f32_plane_stride(int PR, int PC) {
     return r <= 32 ? p + (32 - r) : p + (96 - r);
 }
 
-union Pack8 {
-    uint4 v;
-    uint16_t h[8];
-};
 
 template <int OB>
 __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
@@ -295,6 +290,8 @@ static int lds_bytes_for(const IgemmArgs& a, int dtype, int CC, int OB) {
 }
 
 bool igemm_plan(IgemmArgs& a, int dtype) {
+    a.kind = 0;
+    if (dtype == 1 && igemm_wreg_plan(a)) return true;
     a.OB = a.Cout <= 32 ? 32 : 64;
     // channel-chunk candidates, widest first: the channel count itself (rounded
     // to the k-granularity) when it is small, then powers of two
@@ -321,6 +318,7 @@ bool igemm_plan(IgemmArgs& a, int dtype) {
 }
 
 hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
+    if (a.kind == 1) return launch_igemm_wreg(a, s);
     const int nvb = (a.Vo + kBW - 1) / kBW, nub = (a.Uo + kBH - 1) / kBH;
     dim3 grid(nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
     dim3 block(kThreads);

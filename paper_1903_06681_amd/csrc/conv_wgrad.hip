@@ -30,23 +30,16 @@
 #include <algorithm>
 #include <cstring>
 
+#include "bf16util.h"
 #include "kernels.h"
 
 namespace dc {
 
-typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
-typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
 
 static constexpr int kThreads = 256;
 static constexpr int kBQ = 64;          // output columns staged per step
 static constexpr int kTargetWGs = 256;  // workgroups aimed for per launch (one per CU)
 
-union Pack8 {
-    uint4 v;
-    uint32_t d[4];
-    uint16_t h[8];
-    bf16x8 b;
-};
 
 // ---------------------------------------------------------------- planning
 
@@ -75,11 +68,17 @@ struct Plan {
 };
 
 static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, int stride,
-                      int Hot, int Wot, Plan* pl) {
+                      int Hot, int Wot, int base_c, Plan* pl) {
     std::memset(pl, 0, sizeof(*pl));
-    if (dtype == 1 && stride == 1 && S <= 7) {
+    const bool xcol_aligned = base_c % 8 == 0;   // strip staging reads whole 16-byte x chunks
+    if (dtype == 1 && stride == 1 && S <= 7 && xcol_aligned) {
         pl->kind = WGRAD_STRIP_BF16;
-        pl->TRB = std::min(bf16_trb(S), R);
+        // filter rows per workgroup: the largest divisor of R that fits the
+        // accumulators (rows x S <= 9 tiles of 32x32), so every group is full
+        int trb = 1;
+        for (int d = 1; d <= std::min(bf16_trb(S), R); ++d)
+            if (R % d == 0) trb = d;
+        pl->TRB = trb;
         pl->gy = (R + pl->TRB - 1) / pl->TRB;
         pl->gz = ((K + 63) / 64) * ((C + 63) / 64);
         pl->nqb = (Wot + kBQ - 1) / kBQ;
@@ -89,9 +88,7 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
         pl->rows_per_seg = (Hot + nseg - 1) / nseg;
         pl->nseg = (Hot + pl->rows_per_seg - 1) / pl->rows_per_seg;
         pl->nchunks = strips * pl->nseg;
-        // template capacity: filter rows x S taps per wave
-        const int trb_cap = S == 1 ? 9 : std::max(1, 9 / S);
-        pl->F = int64_t(pl->gy) * pl->gz * 4 * trb_cap * S * 1024;
+        pl->F = int64_t(pl->gy) * pl->gz * 4 * pl->TRB * S * 1024;
         pl->frag = 1;
         return true;
     }
@@ -120,15 +117,15 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
 }
 
 size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
-                             int stride, int Hot, int Wot) {
+                             int stride, int Hot, int Wot, int base_c) {
     Plan pl;
-    if (!make_plan(dtype, ntiles, N, C, K, R, S, stride, Hot, Wot, &pl)) return 0;
+    if (!make_plan(dtype, ntiles, N, C, K, R, S, stride, Hot, Wot, base_c, &pl)) return 0;
     return size_t(pl.nchunks) * size_t(pl.F) * sizeof(float);
 }
 
 bool wgrad_plan(WgradArgs& a, int dtype) {
     Plan pl;
-    if (!make_plan(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.istr, a.Hot, a.Wot, &pl))
+    if (!make_plan(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.istr, a.Hot, a.Wot, a.base_c, &pl))
         return false;
     a.kind = pl.kind; a.gy = pl.gy; a.gz = pl.gz; a.TRB = pl.TRB; a.nchunks = pl.nchunks;
     a.chunks_per_tile = pl.chunks_per_tile; a.rows_per_chunk = pl.rows_per_chunk;
@@ -150,67 +147,10 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
 
 // ---------------------------------------------------------------- strip kernel (bf16)
 
-// Elements [sh, sh+8) of the 16-element window d[0..7] (two aligned 16-byte chunks).
-template <int SH>
-__device__ __forceinline__ uint4 window8(const uint32_t (&d)[8]) {
-    uint4 r;
-    uint32_t* o = reinterpret_cast<uint32_t*>(&r);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        if ((SH & 1) == 0)
-            o[i] = d[SH / 2 + i];
-        else
-            o[i] = __builtin_amdgcn_alignbyte(d[SH / 2 + i + 1], d[SH / 2 + i], 2);
-    }
-    return r;
-}
-
-__device__ __forceinline__ uint4 window8_rt(const uint32_t (&d)[8], int sh) {
-    switch (sh) {
-        case 0: return window8<0>(d);
-        case 1: return window8<1>(d);
-        case 2: return window8<2>(d);
-        case 3: return window8<3>(d);
-        case 4: return window8<4>(d);
-        case 5: return window8<5>(d);
-        case 6: return window8<6>(d);
-        default: return window8<7>(d);
-    }
-}
-
-// 8 consecutive bf16 of a row starting at column g (any alignment); zero for
-// columns outside [0, ncols).  row is 16-byte aligned and has `pitch` (a
-// multiple of 8) readable elements.
-__device__ __forceinline__ uint4 load_row8(const uint16_t* row, int g, int ncols, int pitch,
-                                           bool row_ok) {
-    uint4 z = make_uint4(0, 0, 0, 0);
-    if (!row_ok || g >= ncols) return z;
-    const int ga = g & ~7, sh = g - ga;
-    uint4 v0 = (ga < pitch) ? *reinterpret_cast<const uint4*>(row + ga) : z;
-    uint4 v;
-    if (sh == 0) {
-        v = v0;
-    } else {
-        uint4 v1 = (ga + 8 < pitch) ? *reinterpret_cast<const uint4*>(row + ga + 8) : z;
-        const uint32_t d[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-        v = window8_rt(d, sh);
-    }
-    const int nv = ncols - g;   // valid elements in this group of 8
-    if (nv < 8) {
-        uint32_t* w = reinterpret_cast<uint32_t*>(&v);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            uint32_t m = (2 * i < nv ? 0x0000ffffu : 0u) | (2 * i + 1 < nv ? 0xffff0000u : 0u);
-            w[i] &= m;
-        }
-    }
-    return v;
-}
-
 template <int SS, int TRB>
 __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int NR = a.TRB + 1;                               // x ring slots
+    constexpr int NR = TRB + 1;                             // x ring slots
     uint16_t* xring = reinterpret_cast<uint16_t*>(smem);    // [NR][64 ci][kXP]
     uint16_t* dyb = xring + NR * 64 * kXP;                  // [2][64 o][kXP]
 
@@ -222,8 +162,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
     const int p0 = seg * a.rows_per_seg;
     const int nrows = min(a.rows_per_seg, a.Hot - p0);
     const int q0 = qb * kBQ;
-    const int r0 = blockIdx.y * a.TRB;
-    const int nTR = min(a.TRB, a.R - r0);
+    const int r0 = blockIdx.y * TRB;
+    constexpr int nTR = TRB;                      // the plan makes every row group full
     const int ncsb = (a.C + 63) / 64;
     const int o0 = (blockIdx.z / ncsb) * 64, c0 = (blockIdx.z % ncsb) * 64;
 
@@ -242,57 +182,73 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
     const int dyg0 = q0 + a.dy_off;                // global column of staged dy column 0
     const int dy_end = a.dy_off + a.Wot;           // dy interior ends here
     const int xrow0 = p0 + a.base_r + r0;          // x row of ring row 0
+    const int dysh = dyg0 & 7, dya0 = dyg0 - dysh;
 
     // staging units: x row = 64 channels x 9 groups of 8; dy row = 64 filters x 8 groups
     constexpr int XU = 64 * 9, DU = 64 * 8;
     constexpr int XPT = (XU + kThreads - 1) / kThreads, DPT = DU / kThreads;
-    uint4 xv[XPT], dv[DPT];
+    // Staging in two phases so that global loads overlap the MFMAs:
+    // load_*() only issues unconditional 16-byte loads from clamped addresses
+    // into registers; store_*() (after the next row's MFMAs) shifts the
+    // misaligned dy chunks, zeroes everything outside the tile and writes LDS.
+    // Two register buffers: the data of step j (x row j+nTR-1, dy row j) is
+    // loaded at the start of step j-2 and stored to LDS at the end of step j-1.
+    struct Regs {
+        uint4 x[XPT];
+        uint4 d0[DPT], d1[DPT];
+    };
+    Regs bufA, bufB;
 
-    auto load_x = [&](int m) {   // ring row m -> registers
+    auto load_x = [&](int m, Regs& r) {   // ring row m -> registers
+        const int gr = min(max(xrow0 + m, 0), a.x_rows - 1);
+#pragma unroll
+        for (int k = 0; k < XPT; ++k) {
+            const int u = min(tid + k * kThreads, XU - 1);
+            const int ci = u / 9, g8 = u - ci * 9;
+            const int gc = min(xg0 + 8 * g8, a.x_pitch - 8);
+            r.x[k] = *reinterpret_cast<const uint4*>(xt + min(c0 + ci, a.C - 1) * xplane +
+                                                     int64_t(gr) * a.x_pitch + gc);
+        }
+    };
+    auto store_x = [&](int m, Regs& r) {
+        uint16_t* slot = xring + (m % NR) * 64 * kXP;
         const int gr = xrow0 + m;
         const bool rok = gr >= 0 && gr < a.x_rows;
 #pragma unroll
         for (int k = 0; k < XPT; ++k) {
             const int u = tid + k * kThreads;
-            xv[k] = make_uint4(0, 0, 0, 0);
             if (u < XU) {
                 const int ci = u / 9, g8 = u - ci * 9;
-                if (c0 + ci < a.C)
-                    xv[k] = load_row8(xt + (c0 + ci) * xplane + int64_t(gr) * a.x_pitch,
-                                      xg0 + 8 * g8, a.x_cols, a.x_pitch, rok);
+                const int nv = (rok && c0 + ci < a.C) ? a.x_cols - (xg0 + 8 * g8) : 0;
+                *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = mask8(r.x[k], nv);
             }
         }
     };
-    auto store_x = [&](int m) {
-        uint16_t* slot = xring + (m % NR) * 64 * kXP;
-#pragma unroll
-        for (int k = 0; k < XPT; ++k) {
-            const int u = tid + k * kThreads;
-            if (u < XU) {
-                const int ci = u / 9, g8 = u - ci * 9;
-                *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = xv[k];
-            }
-        }
-    };
-    auto load_dy = [&](int i) {   // output row p0 + i -> registers
+    auto load_dy = [&](int i, Regs& r) {   // output row p0 + i -> registers
         const int gr = p0 + i + a.dy_off;
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
             const int u = tid + k * kThreads;
             const int o = u >> 3, g8 = u & 7;
-            dv[k] = make_uint4(0, 0, 0, 0);
-            if (o0 + o < a.K)
-                dv[k] = load_row8(dyt + (o0 + o) * dyplane + int64_t(gr) * a.dy_pitch,
-                                  dyg0 + 8 * g8, dy_end, a.dy_pitch, true);
+            const uint16_t* row = dyt + min(o0 + o, a.K - 1) * dyplane + int64_t(gr) * a.dy_pitch;
+            const int ga = dya0 + 8 * g8;
+            r.d0[k] = *reinterpret_cast<const uint4*>(row + min(ga, a.dy_pitch - 8));
+            if (dysh != 0) r.d1[k] = *reinterpret_cast<const uint4*>(row + min(ga + 8, a.dy_pitch - 8));
         }
     };
-    auto store_dy = [&](int i) {
+    auto store_dy = [&](int i, Regs& r) {
         uint16_t* slot = dyb + (i & 1) * 64 * kXP;
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
             const int u = tid + k * kThreads;
             const int o = u >> 3, g8 = u & 7;
-            *reinterpret_cast<uint4*>(slot + o * kXP + 8 * g8) = dv[k];
+            uint4 v = r.d0[k];
+            if (dysh != 0) {
+                const uint32_t d[8] = {v.x, v.y, v.z, v.w, r.d1[k].x, r.d1[k].y, r.d1[k].z, r.d1[k].w};
+                v = window8_rt(d, dysh);
+            }
+            const int nv = (o0 + o < a.K) ? dy_end - (dyg0 + 8 * g8) : 0;
+            *reinterpret_cast<uint4*>(slot + o * kXP + 8 * g8) = mask8(v, nv);
         }
     };
 
@@ -304,31 +260,41 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    // prologue: the filter rows of the first output row, and its dy row
-    for (int m = 0; m < nTR; ++m) {
-        load_x(m);
-        store_x(m);
+    // prologue: the filter rows of the first output row and its dy row (two
+    // rows in flight at a time), then the loads of step 1 into buffer B
+    load_dy(0, bufA);
+    for (int m = 0; m < nTR; m += 2) {
+        load_x(m, bufA);
+        if (m + 1 < nTR) load_x(m + 1, bufB);
+        store_x(m, bufA);
+        if (m + 1 < nTR) store_x(m + 1, bufB);
     }
-    load_dy(0);
-    store_dy(0);
+    store_dy(0, bufA);
+    if (nrows > 1) {
+        load_x(nTR, bufB);
+        load_dy(1, bufB);
+    }
     __syncthreads();
 
-    const int qmax = min(kBQ, a.Wot - q0);
-    for (int i = 0; i < nrows; ++i) {
-        const bool more = i + 1 < nrows;
-        if (more) {           // next row's data in flight during this row's MFMAs
-            load_x(i + nTR);
-            load_dy(i + 1);
+    auto step = [&](int i, Regs& cur, Regs& nxt) {
+        if (i + 2 < nrows) {   // step i+2's data: two steps of MFMAs to arrive
+            load_x(i + 1 + nTR, cur);
+            load_dy(i + 2, cur);
         }
         const uint16_t* dyrow = dyb + (i & 1) * 64 * kXP + (ow * 32 + l32) * kXP;
-        for (int kq = 0; kq < qmax; kq += 16) {
+        const uint16_t* xrows[TRB];
+#pragma unroll
+        for (int tr = 0; tr < TRB; ++tr)
+            xrows[tr] = xring + ((i + tr) % NR) * 64 * kXP + (cw * 32 + l32) * kXP;
+        // all 64 staged columns: those past the tile have zero dy
+#pragma unroll
+        for (int kq = 0; kq < kBQ; kq += 16) {
             const int qc = kq + 8 * hi;
             Pack8 A;
             A.v = *reinterpret_cast<const uint4*>(dyrow + qc);
 #pragma unroll
             for (int tr = 0; tr < TRB; ++tr) {
-                if (tr >= nTR) continue;
-                const uint16_t* xr = xring + ((i + tr) % NR) * 64 * kXP + (cw * 32 + l32) * kXP;
+                const uint16_t* xr = xrows[tr];
                 Pack8 lo, hh;
                 lo.v = *reinterpret_cast<const uint4*>(xr + qc);
                 hh.v = *reinterpret_cast<const uint4*>(xr + qc + 8);
@@ -344,11 +310,15 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
                 }
             }
         }
-        if (more) {
-            store_x(i + nTR);
-            store_dy(i + 1);
+        if (i + 1 < nrows) {   // step i+1's data, loaded during step i-1
+            store_x(i + nTR, nxt);
+            store_dy(i + 1, nxt);
         }
         __syncthreads();
+    };
+    for (int i = 0; i < nrows; i += 2) {
+        step(i, bufA, bufB);
+        if (i + 1 < nrows) step(i + 1, bufB, bufA);
     }
 
     // partial in fragment order: [chunk][gy][gz][wave][tr][s][16][64]
@@ -356,7 +326,6 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
                   ((int64_t(blockIdx.y) * a.gz + blockIdx.z) * 4 + wave) * TRB * SS * 1024;
 #pragma unroll
     for (int tr = 0; tr < TRB; ++tr) {
-        if (tr >= nTR) continue;
 #pragma unroll
         for (int s = 0; s < SS; ++s)
 #pragma unroll
@@ -628,8 +597,18 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
     const int64_t f = int64_t(blockIdx.x) * 64 + (threadIdx.x & 63);
     const int g = threadIdx.x >> 6;
     float sum = 0.f;
-    if (f < a.F)
-        for (int c = g; c < a.nchunks; c += 4) sum += a.part[int64_t(c) * a.F + f];
+    if (f < a.F) {
+        const float* src = a.part + f;
+        int c = g;
+        for (; c + 28 < a.nchunks; c += 32) {   // eight loads in flight, summed in chunk order
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = src[int64_t(c + 4 * j) * a.F];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sum += v[j];
+        }
+        for (; c < a.nchunks; c += 4) sum += src[int64_t(c) * a.F];
+    }
     red[g][threadIdx.x & 63] = sum;
     __syncthreads();
     if (g != 0 || f >= a.F) return;
@@ -639,12 +618,11 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
     if (a.frag) {
         // [gy][gz][wave][tr][s][16][64] -> (o, ci, r, s)
         const int SS = a.S;
-        const int trb_cap = a.S == 1 ? 9 : max(1, 9 / a.S);
         int64_t t = f;
         const int lane = int(t % 64); t /= 64;
         const int e = int(t % 16); t /= 16;
         const int s = int(t % SS); t /= SS;
-        const int tr = int(t % trb_cap); t /= trb_cap;
+        const int tr = int(t % a.TRB); t /= a.TRB;
         const int wave = int(t % 4); t /= 4;
         const int bz = int(t % a.gz);
         const int by = int(t / a.gz);
@@ -688,17 +666,15 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
     dim3 grid(a.nchunks, a.gy, a.gz);
     hipError_t e = hipErrorInvalidValue;
     if (a.kind == WGRAD_STRIP_BF16) {
-        // the accumulator capacity (TRB rows x S taps) is fixed per filter width
-        switch (a.S) {
-            case 1: e = launch_strip<1, 9>(a, grid, s); break;
-            case 2: e = launch_strip<2, 4>(a, grid, s); break;
-            case 3: e = launch_strip<3, 3>(a, grid, s); break;
-            case 4: e = launch_strip<4, 2>(a, grid, s); break;
-            case 5: e = launch_strip<5, 1>(a, grid, s); break;
-            case 6: e = launch_strip<6, 1>(a, grid, s); break;
-            case 7: e = launch_strip<7, 1>(a, grid, s); break;
-            default: return hipErrorInvalidValue;
-        }
+        // one instantiation per (filter width, filter rows per workgroup)
+#define DC_STRIP(ss, trb) \
+        if (a.S == ss && a.TRB == trb) e = launch_strip<ss, trb>(a, grid, s); else
+        DC_STRIP(1, 1) DC_STRIP(1, 2) DC_STRIP(1, 3) DC_STRIP(1, 4) DC_STRIP(1, 5) DC_STRIP(1, 6)
+        DC_STRIP(1, 7) DC_STRIP(1, 8) DC_STRIP(1, 9) DC_STRIP(2, 1) DC_STRIP(2, 2) DC_STRIP(2, 3)
+        DC_STRIP(2, 4) DC_STRIP(3, 1) DC_STRIP(3, 2) DC_STRIP(3, 3) DC_STRIP(4, 1) DC_STRIP(4, 2)
+        DC_STRIP(5, 1) DC_STRIP(6, 1) DC_STRIP(7, 1)
+        return hipErrorInvalidValue;
+#undef DC_STRIP
     } else if (a.kind == WGRAD_ROWS_BF16) {
         switch (a.S) {
             case 1: e = launch_rows_bf16<1>(a, grid, s); break;

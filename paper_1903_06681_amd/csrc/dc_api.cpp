@@ -178,7 +178,8 @@ static void igemm_common(const Geo& g, int32_t tile, IgemmArgs& a) {
     std::memset(&a, 0, sizeof(a));
     a.ntiles = tile == DC_ALL_TILES ? g.ntiles : 1;
     a.Nn = g.N;
-    a.S = g.S;
+    a.R = g.R; a.S = g.S;
+    a.wK = g.K; a.wC = g.C;
 }
 
 }  // namespace dc
@@ -298,6 +299,7 @@ dc_status dc_conv_fwd(const dc_problem* prob, int32_t tile, const void* x_pad,
     a.base_r = g.h - g.pad; a.base_c = g.h - g.pad;
     a.wr0 = 0; a.wrstep = 1; a.ws0 = 0; a.wsstep = 1;
     a.w_os = int64_t(g.C) * g.R * g.S; a.w_cs = int64_t(g.R) * g.S;
+    a.wmode = 0;
     if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
     return launched(launch_igemm(a, g.dtype, static_cast<hipStream_t>(stream)));
 }
@@ -339,6 +341,7 @@ dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_
             a.ws0 = rc + st_ * (a.Ts - 1); a.wsstep = -st_;
             if (a.Tr == 0 || a.Ts == 0) { a.Tr = 0; a.Ts = 0; a.base_r = 0; a.base_c = 0; }
             a.w_os = int64_t(g.R) * g.S; a.w_cs = int64_t(g.C) * g.R * g.S;
+            a.wmode = 1;
             if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
             dc_status r = launched(launch_igemm(a, g.dtype, s));
             if (r != DC_OK) return r;
@@ -351,7 +354,8 @@ size_t dc_bwd_filter_workspace_bytes(const dc_problem* prob, int32_t tile) {
     Geo g;
     if (make_geo_tile(prob, tile, &g) != DC_OK) return 0;
     int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
-    return wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot);
+    return wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot,
+                                 g.h - g.pad);
 }
 
 dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x_pad,
@@ -364,7 +368,8 @@ dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x
     if (!x_pad || !dy_pad || !dw) return DC_ERR_NULL;
     if (misaligned(x_pad) || misaligned(dy_pad) || misaligned(dw)) return DC_ERR_ALIGN;
     const int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
-    size_t need = wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot);
+    size_t need = wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot,
+                                 g.h - g.pad);
     if (need > 0 && (!workspace || workspace_bytes < need)) return DC_ERR_WORKSPACE;
     if (need > 0 && misaligned(workspace)) return DC_ERR_ALIGN;
     WgradArgs a;

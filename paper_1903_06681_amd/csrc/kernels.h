@@ -60,11 +60,15 @@ struct IgemmArgs {
     int Tr, Ts;
     int base_r, base_c;
     int wr0, wrstep, ws0, wsstep;
-    int S;                       // filter width (weight index stride of r)
+    int R, S;                    // filter height, width of w
     int64_t w_os, w_cs;          // weight strides of o and ci
+    int wK, wC;                  // w is [wK][wC][R][S]
+    int wmode;                   // 0: o indexes wK, ci indexes wC (forward); 1: swapped (backward-data)
     int CC;                      // channels per LDS chunk (multiple of 8 for bf16, 2 for fp32)
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
+    int kind;                    // 0: chunked kernel; 1: register-weight strip kernel
+    int nvb, nseg, rows_per_seg; // strip kernel: 64-column strips, row segments
 };
 
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
@@ -73,6 +77,8 @@ int device_lds_limit();
 // Chooses the channel chunk and LDS size; returns false if no variant fits.
 bool igemm_plan(IgemmArgs& a, int dtype);
 hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s);
+bool igemm_wreg_plan(IgemmArgs& a);
+hipError_t launch_igemm_wreg(const IgemmArgs& a, hipStream_t s);
 
 // ----------------------------------------------------- weight gradient
 //
@@ -111,7 +117,7 @@ struct WgradArgs {
 };
 
 size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
-                             int stride, int Hot, int Wot);
+                             int stride, int Hot, int Wot, int base_c);
 bool wgrad_plan(WgradArgs& a, int dtype);
 hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s);
 
