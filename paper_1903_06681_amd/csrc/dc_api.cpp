@@ -120,29 +120,6 @@ static dc_status launched(hipError_t e) {
 
 // ---------------------------------------------------------------- halo
 
-// Region table of the packed halo format: order N, S, W, E, NW, NE, SW, SE.
-static void halo_regions(int Ht, int Wt, int h, int planes, bool unpack, HaloRegion reg[8]) {
-    static const int di[8] = {-1, 1, 0, 0, -1, -1, 1, 1};
-    static const int dj[8] = {0, 0, -1, 1, -1, 1, -1, 1};
-    static const int opp[8] = {1, 0, 3, 2, 7, 6, 5, 4};
-    int64_t off = 0;
-    for (int d = 0; d < 8; ++d) {
-        HaloRegion& r = reg[d];
-        r.rows = di[d] == 0 ? Ht : h;
-        r.cols = dj[d] == 0 ? Wt : h;
-        r.off = off;
-        off += int64_t(planes) * r.rows * r.cols;
-        r.di = di[d]; r.dj = dj[d]; r.opp = opp[d];
-        if (!unpack) {  // band of the owned block next to neighbour d
-            r.tr0 = di[d] < 0 ? h : (di[d] > 0 ? Ht : h);
-            r.tc0 = dj[d] < 0 ? h : (dj[d] > 0 ? Wt : h);
-        } else {        // margin on side d
-            r.tr0 = di[d] < 0 ? 0 : (di[d] > 0 ? h + Ht : h);
-            r.tc0 = dj[d] < 0 ? 0 : (dj[d] > 0 ? h + Wt : h);
-        }
-    }
-}
-
 static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which,
                              const void* src, void* dst, bool unpack, void* stream) {
     Geo g;
@@ -163,11 +140,11 @@ static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which
     a.planes = g.N * ch;
     a.rows = x ? g.x_rows : g.dy_rows;
     a.pitch = x ? g.x_pitch : g.dy_pitch;
+    a.ht = Ht; a.wt = Wt; a.h = g.h;
     a.P = g.P; a.Q = g.Q;
     a.all_tiles = tile == DC_ALL_TILES;
     a.tile0 = a.all_tiles ? 0 : tile;
     a.ntiles = a.all_tiles ? g.ntiles : 1;
-    halo_regions(Ht, Wt, g.h, a.planes, unpack, a.reg);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return launched(unpack ? launch_halo_unpack(a, g.esize, s) : launch_halo_pack(a, g.esize, s));
 }

@@ -11,14 +11,9 @@ namespace dc {
 
 // ---------------------------------------------------------------- halo
 
-struct HaloRegion {
-    int rows, cols;      // region extent
-    int64_t off;         // element offset of the region in one packed buffer
-    int tr0, tc0;        // region origin in the padded tile (pack: source; unpack: margin)
-    int di, dj;          // direction of the neighbour
-    int opp;             // index of the opposite direction
-};
-
+// Packed halo format: eight regions, order N, S, W, E, NW, NE, SW, SE, each
+// [planes][rows][cols] with rows = h (N/S/corners) or Ht, cols = h (W/E/corners)
+// or Wt, at offsets given by the prefix sums of those sizes.
 struct HaloArgs {
     const void* src;     // pack: padded tiles; unpack: packed buffers
     void* dst;           // pack: packed buffers; unpack: padded tiles
@@ -26,11 +21,11 @@ struct HaloArgs {
     int64_t halo_elems;  // elements per packed buffer
     int planes;          // N * channels
     int rows, pitch;     // padded tile rows and row pitch
+    int ht, wt, h;       // tile extent and margin width
     int P, Q;
     int tile0;           // first tile handled by this launch
     int ntiles;          // tiles handled by this launch
     int all_tiles;       // unpack: read neighbours' send buffers directly
-    HaloRegion reg[8];
 };
 
 hipError_t launch_halo_pack(const HaloArgs& a, int esize, hipStream_t s);
