@@ -14,7 +14,10 @@ The neighbours' halo regions (what the exchange would deliver) are prepared
 once before timing; the transport itself is not part of a GPU's compute.
 All inputs are resident in device memory when timing starts.
 
-value = (forward + backward-data + backward-filter flops) / step time, TFLOP/s.
+value = (forward + backward-data + backward-filter flops) / step time, TFLOP/s,
+with the step time from K whole steps between two events.  Each pass is then
+timed on its own (K back-to-back calls between two events on the launch
+stream); `roofline` reports the slowest convolution pass against its bound.
 Prints one JSON line.  Only one GPU is supported (--gpus 1).
 """
 import argparse
@@ -57,6 +60,44 @@ def algorithmic(L):
         "pack_dy": {"flops": 0, "bytes": 2 * hy},
         "unpack_dy": {"flops": 0, "bytes": 2 * hy},
     }
+
+
+def source_digest():
+    """sha256 over the library's kernel and host sources: changes with any kernel change."""
+    import hashlib
+
+    d = os.path.join(ROOT, "paper_1903_06681_amd", "csrc")
+    hsh = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            hsh.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                hsh.update(fh.read())
+    return hsh.hexdigest()
+
+
+def measured_traffic(kernel, workload, tile):
+    """HBM bytes per launch from a committed counter summary, or None.
+
+    The summary (profiles/<kernel>_<workload>_hbm_traffic.txt) holds `key: value`
+    lines written from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) scaled
+    by the same counters over a copy kernel of known size.  It is used only if
+    it was taken on this tile and on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith(("#", " ", "|", "`")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    try:
+        if kv.get("source_sha256") != source_digest() or int(kv.get("tile", -1)) != tile:
+            return None
+        return int(float(kv["traffic_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(L, x, w, dy, tile, seconds):
@@ -114,6 +155,19 @@ def cpu_baseline(L, x, w, dy, tile, seconds):
     }
 
 
+def copy_calibration(mib):
+    """dst = src * 1 over MIB MiB of fp32: reads and writes exactly MIB MiB each."""
+    import torch
+
+    n = mib * 1024 * 1024 // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,8 +176,11 @@ def main():
     ap.add_argument("--workload", default=None, help="layer name in workloads.LAYERS")
     ap.add_argument("--tile", type=int, default=None, help="tile index (default: an interior tile)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=24.0)
     ap.add_argument("--cold", action="store_true", help="also time steps after a cache flush")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain elementwise copy of MIB MiB a few times (the known-size "
+                         "kernel against which HBM byte counters are scaled) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU's tile; runs on more than one GPU are not supported "
@@ -132,6 +189,9 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_calibration:
+        return copy_calibration(args.copy_calibration)
 
     import harness as H
     import paper_1903_06681_amd as dc
@@ -187,31 +247,39 @@ def main():
         lambda: dc.conv_bwd_data(p, tile, dyp, wd, dx, sh),
     ]
 
-    def step(events=None):
-        for i, c in enumerate(calls):
-            if events is not None:
-                events[i].record(stream)
+    def step():
+        for c in calls:
             c()
-        if events is not None:
-            events[len(calls)].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
-          for _ in range(args.steps)]
+    # timed region 1: K whole steps, nothing else on the stream
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record(stream)
-    for k in range(args.steps):
-        step(ev[k])
+    for _ in range(args.steps):
+        step()
     t1.record(stream)
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_per_step = total_ms / args.steps
-    per_call = {n: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
-                for i, n in enumerate(names)}
+
+    # timed region 2: each pass K times back to back between two events on the
+    # launch stream -> its average launch duration (an event pair around every
+    # single call would add the event markers' own cost to each call)
+    per_call = {}
+    for n, c in zip(names, calls):
+        c()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            c()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        per_call[n] = e0.elapsed_time(e1) / args.steps
 
     alg = algorithmic(L)
     flops_step = 3 * L.flops_per_pass_tile()
@@ -246,6 +314,8 @@ def main():
                     "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4), "traffic": None}
     roofline["kernel"] = {"fwd": "dc_conv_fwd", "bwd_data": "dc_conv_bwd_data",
                           "bwd_filter": "dc_conv_bwd_filter"}[dom]
+    roofline["traffic"] = measured_traffic(roofline["kernel"], L.name, tile)
+    roofline["algorithmic_bytes"] = a["bytes"]
 
     out = {
         "metric": METRIC,
