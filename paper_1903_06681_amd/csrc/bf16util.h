@@ -6,11 +6,52 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 namespace dc {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float floatx16;
+
+// v_mfma_f32_32x32x16_bf16 written out so that the register class of the A
+// operand is chosen here: AG = true reads it from AGPRs (the 512-entry
+// register file of a wave holds a weight operand larger than the 256 VGPRs
+// that way), ZERO = true starts a new accumulation (C = 0).  The accumulator
+// lives in AGPRs.  The hardware interlocks back-to-back MFMAs that accumulate
+// into the same registers; any other reader of the accumulator must come after
+// mfma_drain(), and an A/B operand must not be written by a VALU instruction
+// in the two instructions before the MFMA (A/B here come from loads).  The
+// statements are volatile: memory operations keep their source order around
+// them, which fixes how far loads run ahead and where stores interleave.
+template <bool AG, bool ZERO>
+__device__ __forceinline__ void mfma32x32x16(floatx16& acc, const bf16x8& a, const bf16x8& b) {
+    if constexpr (ZERO) {
+        if constexpr (AG)
+            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&a"(acc) : "a"(a), "v"(b));
+        else
+            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&a"(acc) : "v"(a), "v"(b));
+    } else {
+        if constexpr (AG)
+            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "a"(a), "v"(b));
+        else
+            asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+    }
+}
+
+// Wait states between the last MFMA writing `acc` and any non-MFMA reader of
+// it (32 >= passes + 4 for every 32x32 shape).
+__device__ __forceinline__ void mfma_drain(floatx16& acc) {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" : "+a"(acc));
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
 
 union Pack8 {
     uint4 v;

@@ -51,6 +51,10 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     constexpr int NCG8 = CIN / 8;
     constexpr int BLK_ROW = NCG8 * RPX8;      // 8x8 staging blocks per ring row
     constexpr int BPT = (2 * BLK_ROW + kWThreads - 1) / kWThreads;
+    // weight fragments held in AGPRs (fragment f = k * NOB + ob, f < NAG); the
+    // accumulators take 16 * NOB of the 256 AGPRs, the rest of Wf sits in VGPRs
+    constexpr int NAG = (NOB * KS < (256 - 16 * NOB) / 4) ? NOB * KS : (256 - 16 * NOB) / 4;
+    constexpr int kPre = 3;
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
 
@@ -66,92 +70,16 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int l32 = lane & 31, hi = lane >> 5;
 
-    // ---- weights -> A-fragments in VGPRs, in three LDS passes:
-    //  1. the workgroup's block of w, copied in its natural order with
-    //     coalesced 16-byte loads: rows of `rowlen` elements
-    //       forward:       row = output channel o  -> w[o][0..Cin)[R][S]
-    //       backward-data: row = reduction channel -> w[ci][o0..o0+nO)[R][S]
-    //  2. the fragment image [KS][2][OBT][8]: 8 reduction channels of one
-    //     (output channel, tap) per 16-byte entry, zero where o >= Cout;
-    //  3. each wave reads its OB/32 x KS fragments.
-    const int T = a.R * a.S;
-    const int nO = min(OBT, a.Cout - o0);               // valid output channels here
-    const int nrow = a.wmode ? CIN : nO;
-    const int rowlen = a.wmode ? nO * T : CIN * T;
-    const int pitch = rowlen + ((6 - rowlen % 4) % 4);   // pitch % 4 == 2: odd dword stride
-    const int nat_elems = nrow * pitch;
-    uint16_t* nat = lds;                                 // [nrow][pitch]
-    uint16_t* img = lds + ((nat_elems + 7) & ~7);        // [KS][2][OBT][8]
-    {
-        const uint16_t* w = static_cast<const uint16_t*>(a.w);
-        const int64_t row_stride = a.wmode ? int64_t(a.Cout) * T : int64_t(CIN) * T;
-        const int64_t col0 = a.wmode ? int64_t(o0) * T : int64_t(o0) * CIN * T;
-        const bool vec = (rowlen % 8 == 0) && (row_stride % 8 == 0) && (col0 % 8 == 0);
-        if (vec) {
-            const int vpr = rowlen / 8, nv = nrow * vpr;
-            for (int base = 0; base < nv; base += 8 * kWThreads) {
-                uint4 buf[8];
-#pragma unroll
-                for (int b = 0; b < 8; ++b) {
-                    int v = base + b * kWThreads + tid;
-                    v = v < nv ? v : nv - 1;
-                    const int row = v / vpr, cv = v - row * vpr;
-                    buf[b] = *reinterpret_cast<const uint4*>(w + col0 + row * row_stride + cv * 8);
-                }
-#pragma unroll
-                for (int b = 0; b < 8; ++b) {
-                    const int v = base + b * kWThreads + tid;
-                    if (v < nv) {
-                        const int row = v / vpr, cv = v - row * vpr;
-                        uint32_t* dst = reinterpret_cast<uint32_t*>(nat + row * pitch + cv * 8);
-                        dst[0] = buf[b].x; dst[1] = buf[b].y; dst[2] = buf[b].z; dst[3] = buf[b].w;
-                    }
-                }
-            }
-        } else {
-            for (int e = tid; e < nrow * rowlen; e += kWThreads) {
-                const int row = e / rowlen, cl = e - row * rowlen;
-                nat[row * pitch + cl] = w[col0 + row * row_stride + cl];
-            }
-        }
-    }
-    __syncthreads();
-    for (int u = tid; u < KS * 2 * OBT; u += kWThreads) {
-        const int ol = u % OBT, kh = u / OBT;
-        const int h2 = kh & 1, k = kh >> 1;
-        const int t = k / CG, cgi = k - t * CG;
-        const int tr = t / TS, ts = t - tr * TS;
-        const int tn = (a.wr0 + a.wrstep * tr) * a.S + (a.ws0 + a.wsstep * ts);   // tap in w
-        const int ci0 = cgi * 16 + 8 * h2;
-        Pack8 pk;
-        if (ol < nO) {
-            const int base = a.wmode ? ci0 * pitch + ol * T + tn : ol * pitch + ci0 * T + tn;
-            const int step = a.wmode ? pitch : T;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) pk.h[j] = nat[base + j * step];
-        } else {
-            pk.v = make_uint4(0, 0, 0, 0);
-        }
-        *reinterpret_cast<uint4*>(img + u * 8) = pk.v;
-    }
-    __syncthreads();
-    bf16x8 Wf[NOB][KS];
-#pragma unroll
-    for (int ob = 0; ob < NOB; ++ob)
-#pragma unroll
-        for (int k = 0; k < KS; ++k)
-            Wf[ob][k] = *reinterpret_cast<const bf16x8*>(img + ((k * 2 + hi) * OBT + ob * 32 + l32) * 8);
-    __syncthreads();   // the image space becomes the input ring
-
-    // ---- input ring
+    // ---- input ring addressing; the first ring rows are loaded before the
+    // weights so that both latencies overlap
     const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
     const uint16_t* in = static_cast<const uint16_t*>(a.in) + tile * a.in_tile +
                          int64_t(n) * a.Cin * plane;
     const int xr0 = u0 + a.base_r;   // input row of ring row 0 (stride-1 walk)
     const int xc0 = v0 + a.base_c;   // input column of staged pixel 0 (a multiple of 8)
-    uint4 stg[BPT][8];
+    uint4 stg[BPT][8], stg1[BPT][8];
 
-    auto load_rows = [&](int m0, int nrow) {   // ring rows m0 .. m0+nrow-1 -> registers
+    auto load_rows = [&](uint4 (&sg)[BPT][8], int m0, int nrow) {   // ring rows m0 .. m0+nrow-1 -> registers
 #pragma unroll
         for (int b = 0; b < BPT; ++b) {
             const int blk = tid + b * kWThreads;
@@ -166,11 +94,11 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 const uint16_t* src = in + int64_t(gr) * a.in_pitch + gc + (cg8 * 8) * plane;
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
-                    stg[b][j] = *reinterpret_cast<const uint4*>(src + j * plane);
+                    sg[b][j] = *reinterpret_cast<const uint4*>(src + j * plane);
             }
         }
     };
-    auto store_rows = [&](int m0, int nrow) {
+    auto store_rows = [&](const uint4 (&sg)[BPT][8], int m0, int nrow) {
 #pragma unroll
         for (int b = 0; b < BPT; ++b) {
             const int blk = tid + b * kWThreads;
@@ -178,7 +106,7 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 const int m = m0 + blk / BLK_ROW, rb = blk % BLK_ROW;
                 const int cg8 = rb % NCG8, pg = rb / NCG8;
                 uint4 t[8];
-                transpose8x8(stg[b], t);
+                transpose8x8(sg[b], t);
                 uint16_t* dst = lds + (m % NRING) * ROWSZ + (pg * 8) * PS + cg8 * 8;
 #pragma unroll
                 for (int p = 0; p < 8; ++p) *reinterpret_cast<uint4*>(dst + p * PS) = t[p];
@@ -186,57 +114,225 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
         }
     };
 
-    // prologue: ring rows 0 .. TR (the inputs of the first two output rows)
-    for (int m = 0; m <= TR; m += 2) {
+    constexpr int NPRE = 1;   // row pairs loaded before the weights
+    load_rows(stg, 0, min(2, TR + 1));
+    if (NPRE > 1) load_rows(stg1, 2, min(2, TR - 1));
+
+    // ---- weights -> A-fragments, in two passes:
+    //  1. the workgroup's block of w goes to LDS as Wl[o][ci][t'] (rows of
+    //     CIN*T elements, pitch PW), t' the tap in k-step order:
+    //       forward:       Wl[o][ci][t]       = w[o0+o][ci][t]
+    //       backward-data: Wl[o][ci][T-1-t]   = w[ci][o0+o][t]   (flipped taps)
+    //     rows o >= Cout - o0 hold whatever was read: they only feed output
+    //     channels that are never stored;
+    //  2. each lane reads, per (output block, 16-channel group), the 8
+    //     channels x T taps of its row and channel half (16*T contiguous
+    //     bytes) and regroups them in registers into T fragments.
+    constexpr int T = TR * TS;
+    constexpr int RL = CIN * T;                                    // row length
+    constexpr int PW = ((RL * 2 + 239) / 256 * 256 + 16) / 2;      // 2*PW = 16 (mod 256)
+    uint16_t* Wl = lds;
+    {
+        const uint16_t* w = static_cast<const uint16_t*>(a.w);
+        // Every workgroup reads the same block of w at the same moment: start
+        // each one at its own offset so that the requests spread out.
+        const unsigned rot0 = blockIdx.x * 149u + blockIdx.y * 31u;
+        if (a.wvec && a.wmode == 0) {
+            // rows o0 .. o0+OBT-1 of w are consecutive: 16-byte chunks straight to
+            // LDS, all of a thread's loads in flight at once
+            constexpr int CPR = RL / 8, NCH = OBT * CPR, NB = (NCH + kWThreads - 1) / kWThreads;
+            const int rot = int(rot0 % unsigned(NCH));
+            uint4 buf[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                int v = min(b * kWThreads + tid, NCH - 1) + rot;
+                v = v >= NCH ? v - NCH : v;
+                const int o = min(o0 + v / CPR, a.Cout - 1), cc = v % CPR;
+                buf[b] = *reinterpret_cast<const uint4*>(w + int64_t(o) * RL + cc * 8);
+            }
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                int v = b * kWThreads + tid;
+                if (v < NCH) {
+                    v += rot;
+                    v = v >= NCH ? v - NCH : v;
+                    *reinterpret_cast<uint4*>(Wl + (v / CPR) * PW + (v % CPR) * 8) = buf[b];
+                }
+            }
+        } else if (a.wvec) {
+            // row ci of w holds (o, t) of this block as OBT*T consecutive elements
+            constexpr int CPR = OBT * T / 8, NCH = CIN * CPR, NB = (NCH + kWThreads - 1) / kWThreads;
+            const int64_t rs = int64_t(a.Cout) * T;                 // w row stride
+            const int64_t last = int64_t(a.Cout) * T - 8;           // last chunk start in a row
+            const int rot = int(rot0 % unsigned(NCH));
+            uint4 buf[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                int v = min(b * kWThreads + tid, NCH - 1) + rot;
+                v = v >= NCH ? v - NCH : v;
+                const int ci = v / CPR, cc = v % CPR;
+                const int64_t col = min(int64_t(o0) * T + cc * 8, last);
+                buf[b] = *reinterpret_cast<const uint4*>(w + ci * rs + col);
+            }
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                int v = b * kWThreads + tid;
+                if (v < NCH) {
+                    v += rot;
+                    v = v >= NCH ? v - NCH : v;
+                    const int ci = v / CPR, e0 = (v % CPR) * 8;
+                    Pack8 pk;
+                    pk.v = buf[b];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const int o = (e0 + j) / T, t = (e0 + j) % T;
+                        Wl[o * PW + ci * T + (T - 1 - t)] = pk.h[j];
+                    }
+                }
+            }
+        } else {
+            // unaligned rows: element by element
+            for (int e = tid; e < OBT * RL; e += kWThreads) {
+                const int o = e / RL, r = e % RL, ci = r / T, t = r % T;
+                const int oc = min(o0 + o, a.Cout - 1);
+                Wl[o * PW + r] = a.wmode ? w[(int64_t(ci) * a.Cout + oc) * T + (T - 1 - t)]
+                                         : w[(int64_t(oc) * CIN + ci) * T + t];
+            }
+        }
+    }
+    __syncthreads();
+    bf16x8 Wf[NOB][KS];
+    static_for<0, NOB * CG>([&](auto gc) {
+        constexpr int g = decltype(gc)::value, ob = g / CG, cg = g % CG;
+        const uint16_t* row = Wl + (ob * 32 + l32) * PW + (cg * 16 + 8 * hi) * T;
+        uint32_t seg[4 * T];   // element c*T + t: channel c of the 8, tap t
+#pragma unroll
+        for (int m = 0; m < T; ++m) {
+            const uint4 q = *reinterpret_cast<const uint4*>(row + 8 * m);
+            seg[4 * m] = q.x; seg[4 * m + 1] = q.y; seg[4 * m + 2] = q.z; seg[4 * m + 3] = q.w;
+        }
+        static_for<0, T>([&](auto tc) {
+            constexpr int t = decltype(tc)::value;
+            Pack8 p;
+            static_for<0, 4>([&](auto qc) {
+                constexpr int q = decltype(qc)::value;
+                constexpr int e0 = (2 * q) * T + t, e1 = (2 * q + 1) * T + t;
+                const uint32_t lo = (e0 & 1) ? (seg[e0 >> 1] >> 16) : (seg[e0 >> 1] & 0xffffu);
+                const uint32_t hi16 = (e1 & 1) ? (seg[e1 >> 1] & 0xffff0000u) : (seg[e1 >> 1] << 16);
+                p.d[q] = lo | hi16;
+            });
+            Wf[ob][t * CG + cg] = p.b;
+        });
+    });
+    // settle each fragment in its register class before the loop
+    static_for<0, NOB * KS>([&](auto fc) {
+        constexpr int f = decltype(fc)::value;
+        bf16x8& wf = Wf[f % NOB][f / NOB];
+        if constexpr (f < NAG)
+            asm volatile("" : "+a"(wf));
+        else
+            asm volatile("" : "+v"(wf));
+    });
+    __syncthreads();   // the image space becomes the input ring
+
+    // ---- input ring
+    // ring rows 0 .. TR (the inputs of the first two output rows)
+    store_rows(stg, 0, min(2, TR + 1));
+    if (NPRE > 1) store_rows(stg1, 2, min(2, TR - 1));
+    for (int m = 2 * NPRE; m <= TR; m += 2) {
         const int nr = min(2, TR + 1 - m);
-        load_rows(m, nr);
-        store_rows(m, nr);
+        load_rows(stg, m, nr);
+        store_rows(stg, m, nr);
     }
     __syncthreads();
 
-    float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
     const int wrow = wave >> 1;
     const int px = (wave & 1) * 32 + l32;
+    const int v = v0 + px;
     const int nsteps = (u_end - u0 + 1) / 2;
-    for (int i = 0; i < nsteps; ++i) {
-        const bool more = i + 1 < nsteps;
-        if (more) load_rows(2 * i + TR + 1, 2);
-
-        floatx16 acc[NOB];
-#pragma unroll
-        for (int ob = 0; ob < NOB; ++ob)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[ob][e] = 0.f;
-        const int slot0 = (2 * i + wrow) % NRING;
-#pragma unroll
-        for (int k = 0; k < KS; ++k) {
-            const int t = k / CG, cgi = k % CG;
-            const int tr = t / TS, ts = t % TS;
-            int slot = slot0 + tr;
-            if (slot >= NRING) slot -= NRING;
-            const bf16x8 B = *reinterpret_cast<const bf16x8*>(
-                lds + slot * ROWSZ + (px + ts) * PS + cgi * 16 + 8 * hi);
-#pragma unroll
-            for (int ob = 0; ob < NOB; ++ob)
-                acc[ob] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(Wf[ob][k], B, acc[ob], 0, 0, 0);
-        }
-
-        // D layout: value e of lane l is output channel 8*(e/4) + 4*(l/32) + e%4, pixel l%32
-        const int u = u0 + 2 * i + wrow;
-        const int v = v0 + px;
+    const int64_t oplane = int64_t(a.out_rows) * a.out_cols;
+    // output of this lane's pixel at channel o0 + 4*hi; channel o0 + 4*hi + c is c*oplane further
+    float* const out = a.out + tile * a.out_tile + (int64_t(n) * a.Cout + o0 + 4 * hi) * oplane +
+                       int64_t(v) * a.ostr + a.oph_c;
+    // every lane's pixel and every channel of the block in range: stores need no masks
+    const bool block_full = (v0 + 64 <= a.Vo) && (o0 + OBT <= a.Cout);
+    auto out_row = [&](int u) { return out + int64_t(u * a.ostr + a.oph_r) * a.out_cols; };
+    // D layout: value e of lane l is output channel 8*(e/4) + 4*(l/32) + e%4, pixel l%32
+    auto store_masked = [&](const floatx16 (&acc)[NOB], int u) {
         if (u < u_end && v < a.Vo) {
-            float* orow = out + int64_t(u * a.ostr + a.oph_r) * a.out_cols + v * a.ostr + a.oph_c;
+            float* orow = out_row(u);
 #pragma unroll
             for (int ob = 0; ob < NOB; ++ob)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
-                    const int o = o0 + ob * 32 + 8 * (e / 4) + 4 * hi + (e % 4);
-                    if (o < a.Cout) orow[int64_t(o) * a.out_rows * a.out_cols] = acc[ob][e];
+                    const int oc = ob * 32 + 8 * (e / 4) + (e % 4);
+                    if (o0 + 4 * hi + oc < a.Cout) __builtin_nontemporal_store(acc[ob][e], orow + int64_t(oc) * oplane);
                 }
         }
-        if (more) store_rows(2 * i + TR + 1, 2);
+    };
+
+    // One step: two output rows.  The MFMAs of step i are interleaved with the
+    // stores of step i-1's accumulator (`prev`), so the stores drain while the
+    // matrix cores run.  Outputs are written once and not read again here:
+    // non-temporal stores keep them from displacing the inputs in the caches.
+    auto step = [&](int i, floatx16 (&acc)[NOB], const floatx16 (&prev)[NOB]) {
+        const bool more = i + 1 < nsteps;
+        if (more) load_rows(stg, 2 * i + TR + 1, 2);
+        const int slot0 = (2 * i + wrow) % NRING;
+        auto readB = [&](int k) {
+            const int t = k / CG, cgi = k % CG;
+            const int tr = t / TS, ts = t % TS;
+            int slot = slot0 + tr;
+            if (slot >= NRING) slot -= NRING;
+            return *reinterpret_cast<const bf16x8*>(lds + slot * ROWSZ + (px + ts) * PS + cgi * 16 + 8 * hi);
+        };
+        const int u_prev = u0 + 2 * (i - 1) + wrow;
+        const bool fast = i > 0 && block_full && u_prev < u_end;
+        float* const prow = out_row(u_prev);
+        auto mfmas = [&](auto with_stores) {
+            // B operands run kPre k-steps ahead of the MFMAs that consume them
+            bf16x8 Bq[kPre + 1];
+#pragma unroll
+            for (int k = 0; k < kPre && k < KS; ++k) Bq[k] = readB(k);
+            static_for<0, NOB * KS>([&](auto fc) {
+                constexpr int f = decltype(fc)::value, k = f / NOB, ob = f % NOB;
+                if constexpr (ob == 0 && k + kPre < KS) Bq[(k + kPre) % (kPre + 1)] = readB(k + kPre);
+                mfma32x32x16<(f < NAG), (k == 0)>(acc[ob], Wf[ob][k], Bq[k % (kPre + 1)]);
+                // one store per MFMA from the start of the step: the stores have
+                // completed by the wait for the staging loads at the end of it
+                constexpr int s = f;
+                if constexpr (decltype(with_stores)::value && s < 16 * NOB) {
+                    constexpr int sob = s / 16, e = s % 16;
+                    constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
+                    __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+                }
+            });
+        };
+        if (fast)
+            mfmas(std::true_type{});
+        else
+            mfmas(std::false_type{});
+        if (fast && NOB * KS < 16 * NOB) {   // fewer MFMAs than stores: the rest here
+            static_for<NOB * KS, 16 * NOB>([&](auto sc) {
+                constexpr int s = decltype(sc)::value, sob = s / 16, e = s % 16;
+                constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
+                __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+            });
+        }
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob) mfma_drain(acc[ob]);
+        if (i > 0 && !fast) store_masked(prev, u_prev);
+        if (more) store_rows(stg, 2 * i + TR + 1, 2);
         __syncthreads();
+    };
+
+    floatx16 acc[NOB], prev[NOB];
+    for (int i = 0; i < nsteps; ++i) {
+        step(i, acc, prev);
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob) prev[ob] = acc[ob];
     }
+    if (nsteps > 0) store_masked(prev, u0 + 2 * (nsteps - 1) + wrow);
 }
 
 // ---------------------------------------------------------------- planning
@@ -251,14 +347,13 @@ static bool wreg_shape(int NOB, int TR, int TS, int CG) {
     return false;
 }
 
-static int wreg_lds(int NOB, int TR, int TS, int CG, int nO, int T, int wmode) {
+static int wreg_lds(int NOB, int TR, int TS, int CG) {
     const int CIN = CG * 16, PS = 8 * ((CIN / 8) | 1), RPX8 = (64 + TS - 1 + 7) / 8;
     const int ring = (TR + 3) * RPX8 * 8 * PS * 2;
-    const int nrow = wmode ? CIN : nO, rowlen = wmode ? nO * T : CIN * T;
-    const int pitch = rowlen + ((6 - rowlen % 4) % 4);
-    const int nat = ((nrow * pitch + 7) & ~7) * 2;
-    const int image = TR * TS * CG * 2 * NOB * 32 * 16;
-    return ring > nat + image ? ring : nat + image;
+    const int RL = CIN * TR * TS;
+    const int PW = ((RL * 2 + 239) / 256 * 256 + 16) / 2;
+    const int wl = NOB * 32 * PW * 2;
+    return ring > wl ? ring : wl;
 }
 
 bool igemm_wreg_plan(IgemmArgs& a) {
@@ -267,8 +362,15 @@ bool igemm_wreg_plan(IgemmArgs& a) {
     const int NOB = a.Cout <= 32 ? 1 : 2;
     const int CG = a.Cin / 16;
     if (!wreg_shape(NOB, a.Tr, a.Ts, CG)) return false;
-    const int lds = wreg_lds(NOB, a.Tr, a.Ts, CG, a.Cout < NOB * 32 ? a.Cout : NOB * 32, a.R * a.S,
-                             a.wmode);
+    // taps in k-step order: the identity (forward) or the full flip (backward-data, stride 1)
+    if (a.Tr != a.R || a.Ts != a.S) return false;
+    if (a.wmode == 0 && !(a.wr0 == 0 && a.wrstep == 1 && a.ws0 == 0 && a.wsstep == 1)) return false;
+    if (a.wmode == 1 && !(a.wr0 == a.R - 1 && a.wrstep == -1 && a.ws0 == a.S - 1 && a.wsstep == -1))
+        return false;
+    const int T = a.R * a.S;
+    a.wvec = a.wmode ? int((int64_t(a.Cout) * T) % 8 == 0 && (int64_t(a.Cout) * T) >= 8)
+                     : int((int64_t(a.Cin) * T) % 8 == 0);
+    const int lds = wreg_lds(NOB, a.Tr, a.Ts, CG);
     if (lds > device_lds_limit()) return false;
     a.OB = NOB * 32;
     a.nvb = (a.Vo + 63) / 64;

@@ -59,6 +59,7 @@ struct IgemmArgs {
     int64_t w_os, w_cs;          // weight strides of o and ci
     int wK, wC;                  // w is [wK][wC][R][S]
     int wmode;                   // 0: o indexes wK, ci indexes wC (forward); 1: swapped (backward-data)
+    int wvec;                    // weight rows allow 16-byte chunk copies (set by the plan)
     int CC;                      // channels per LDS chunk (multiple of 8 for bf16, 2 for fp32)
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
