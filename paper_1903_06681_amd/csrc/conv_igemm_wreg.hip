@@ -52,8 +52,9 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     constexpr int BLK_ROW = NCG8 * RPX8;      // 8x8 staging blocks per ring row
     constexpr int BPT = (2 * BLK_ROW + kWThreads - 1) / kWThreads;
     // weight fragments held in AGPRs (fragment f = k * NOB + ob, f < NAG); the
-    // accumulators take 16 * NOB of the 256 AGPRs, the rest of Wf sits in VGPRs
-    constexpr int NAG = (NOB * KS < (256 - 16 * NOB) / 4) ? NOB * KS : (256 - 16 * NOB) / 4;
+    // two accumulator sets take 32 * NOB of the 256 AGPRs, the rest of Wf sits
+    // in VGPRs
+    constexpr int NAG = (NOB * KS < (256 - 32 * NOB) / 4) ? NOB * KS : (256 - 32 * NOB) / 4;
     constexpr int kPre = 3;
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* lds = reinterpret_cast<uint16_t*>(smem);
@@ -271,13 +272,21 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
         }
     };
 
-    // One step: two output rows.  The MFMAs of step i are interleaved with the
-    // stores of step i-1's accumulator (`prev`), so the stores drain while the
-    // matrix cores run.  Outputs are written once and not read again here:
-    // non-temporal stores keep them from displacing the inputs in the caches.
+    // One step: two output rows.  Within the MFMA stream of step i go
+    //  - the stores of step i-1's accumulator (`prev`), two per MFMA from the
+    //    start, so they drain while the matrix cores run (outputs are written
+    //    once: non-temporal stores keep them from displacing the inputs);
+    //  - near the end, the transpose and LDS writes of the two input rows that
+    //    step i+1 adds to the ring (loaded at the top of step i) -- their ring
+    //    slots are not read in step i.
+    // Loads and ring writes are unconditional (rows past the segment are
+    // clamped reads, staged into slots no later step reads), so the waits
+    // for them are exact.  The accumulators alternate between two register
+    // sets from step to step.
+    constexpr int NST = 16 * NOB;                       // stores per step
+    constexpr int STAGE_AT = NOB * KS > 8 ? NOB * KS - 8 : 0;
     auto step = [&](int i, floatx16 (&acc)[NOB], const floatx16 (&prev)[NOB]) {
-        const bool more = i + 1 < nsteps;
-        if (more) load_rows(stg, 2 * i + TR + 1, 2);
+        load_rows(stg, 2 * i + TR + 1, 2);
         const int slot0 = (2 * i + wrow) % NRING;
         auto readB = [&](int k) {
             const int t = k / CG, cgi = k % CG;
@@ -289,6 +298,11 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
         const int u_prev = u0 + 2 * (i - 1) + wrow;
         const bool fast = i > 0 && block_full && u_prev < u_end;
         float* const prow = out_row(u_prev);
+        auto store_prev = [&](auto sc) {
+            constexpr int s = decltype(sc)::value, sob = s / 16, e = s % 16;
+            constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
+            __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+        };
         auto mfmas = [&](auto with_stores) {
             // B operands run kPre k-steps ahead of the MFMAs that consume them
             bf16x8 Bq[kPre + 1];
@@ -298,41 +312,37 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 constexpr int f = decltype(fc)::value, k = f / NOB, ob = f % NOB;
                 if constexpr (ob == 0 && k + kPre < KS) Bq[(k + kPre) % (kPre + 1)] = readB(k + kPre);
                 mfma32x32x16<(f < NAG), (k == 0)>(acc[ob], Wf[ob][k], Bq[k % (kPre + 1)]);
-                // one store per MFMA from the start of the step: the stores have
-                // completed by the wait for the staging loads at the end of it
-                constexpr int s = f;
-                if constexpr (decltype(with_stores)::value && s < 16 * NOB) {
-                    constexpr int sob = s / 16, e = s % 16;
-                    constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
-                    __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+                if constexpr (decltype(with_stores)::value && 2 * f < NST) {
+                    store_prev(std::integral_constant<int, 2 * f>{});
+                    store_prev(std::integral_constant<int, 2 * f + 1>{});
                 }
+                if constexpr (f == STAGE_AT) store_rows(stg, 2 * i + TR + 1, 2);
             });
+            if constexpr (decltype(with_stores)::value && 2 * NOB * KS < NST)   // fewer MFMAs than stores
+                static_for<2 * NOB * KS, NST>([&](auto sc) { store_prev(sc); });
         };
         if (fast)
             mfmas(std::true_type{});
         else
             mfmas(std::false_type{});
-        if (fast && NOB * KS < 16 * NOB) {   // fewer MFMAs than stores: the rest here
-            static_for<NOB * KS, 16 * NOB>([&](auto sc) {
-                constexpr int s = decltype(sc)::value, sob = s / 16, e = s % 16;
-                constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
-                __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
-            });
-        }
 #pragma unroll
         for (int ob = 0; ob < NOB; ++ob) mfma_drain(acc[ob]);
         if (i > 0 && !fast) store_masked(prev, u_prev);
-        if (more) store_rows(stg, 2 * i + TR + 1, 2);
         __syncthreads();
     };
 
-    floatx16 acc[NOB], prev[NOB];
-    for (int i = 0; i < nsteps; ++i) {
-        step(i, acc, prev);
-#pragma unroll
-        for (int ob = 0; ob < NOB; ++ob) prev[ob] = acc[ob];
+    floatx16 accA[NOB], accB[NOB];
+    int i = 0;
+    for (; i + 1 < nsteps; i += 2) {
+        step(i, accA, accB);
+        step(i + 1, accB, accA);
     }
-    if (nsteps > 0) store_masked(prev, u0 + 2 * (nsteps - 1) + wrow);
+    if (i < nsteps) {
+        step(i, accA, accB);
+        store_masked(accA, u0 + 2 * i + wrow);
+    } else if (nsteps > 0) {
+        store_masked(accB, u0 + 2 * (i - 1) + wrow);
+    }
 }
 
 // ---------------------------------------------------------------- planning

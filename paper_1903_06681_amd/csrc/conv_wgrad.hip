@@ -224,8 +224,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
             }
         }
     };
-    auto load_dy = [&](int i, Regs& r) {   // output row p0 + i -> registers
-        const int gr = p0 + i + a.dy_off;
+    auto load_dy = [&](int i, Regs& r) {   // output row p0 + i -> registers (clamped)
+        const int gr = min(p0 + i + a.dy_off, dy_rows - 1);
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
             const int u = tid + k * kThreads;
@@ -233,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
             const uint16_t* row = dyt + min(o0 + o, a.K - 1) * dyplane + int64_t(gr) * a.dy_pitch;
             const int ga = dya0 + 8 * g8;
             r.d0[k] = *reinterpret_cast<const uint4*>(row + min(ga, a.dy_pitch - 8));
-            if (dysh != 0) r.d1[k] = *reinterpret_cast<const uint4*>(row + min(ga + 8, a.dy_pitch - 8));
+            r.d1[k] = *reinterpret_cast<const uint4*>(row + min(ga + 8, a.dy_pitch - 8));
         }
     };
     auto store_dy = [&](int i, Regs& r) {
@@ -252,13 +252,17 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
         }
     };
 
+    // accumulators live in AGPRs (the MFMAs are written out, see mfma32x32x16);
+    // the empty statement after zeroing settles them there
     floatx16 acc[TRB][SS];
 #pragma unroll
     for (int i = 0; i < TRB; ++i)
 #pragma unroll
-        for (int j = 0; j < SS; ++j)
+        for (int j = 0; j < SS; ++j) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+            asm volatile("s_nop 2" : "+a"(acc[i][j]));
+        }
 
     // prologue: the filter rows of the first output row and its dy row (two
     // rows in flight at a time), then the loads of step 1 into buffer B
@@ -270,56 +274,108 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
         if (m + 1 < nTR) store_x(m + 1, bufB);
     }
     store_dy(0, bufA);
-    if (nrows > 1) {
-        load_x(nTR, bufB);
-        load_dy(1, bufB);
-    }
+    load_x(nTR, bufB);
+    load_dy(1, bufB);
     __syncthreads();
 
+    // One k-step = 16 pixels: the dy chunk (A) of this lane's filter row and,
+    // per filter row tr, the 8 + (SS - 1) staged x elements from which the SS
+    // shifted windows (B) are cut.  The LDS reads of k-step kq+1 are issued
+    // before the MFMAs of k-step kq.
+    constexpr int XH = SS <= 5 ? 2 : 4;   // dwords read past the first 8 elements
+    struct KData {
+        uint4 A;
+        uint32_t x[TRB][4 + XH];
+    };
+    // Loads and LDS stores are unconditional (rows past the chunk are clamped
+    // reads, staged into slots no later step reads): with no branches around
+    // them the wait for the loads of two steps back leaves the newer ones in
+    // flight.
     auto step = [&](int i, Regs& cur, Regs& nxt) {
-        if (i + 2 < nrows) {   // step i+2's data: two steps of MFMAs to arrive
-            load_x(i + 1 + nTR, cur);
-            load_dy(i + 2, cur);
-        }
         const uint16_t* dyrow = dyb + (i & 1) * 64 * kXP + (ow * 32 + l32) * kXP;
         const uint16_t* xrows[TRB];
 #pragma unroll
         for (int tr = 0; tr < TRB; ++tr)
             xrows[tr] = xring + ((i + tr) % NR) * 64 * kXP + (cw * 32 + l32) * kXP;
-        // all 64 staged columns: those past the tile have zero dy
-#pragma unroll
-        for (int kq = 0; kq < kBQ; kq += 16) {
-            const int qc = kq + 8 * hi;
-            Pack8 A;
-            A.v = *reinterpret_cast<const uint4*>(dyrow + qc);
+        auto read_k = [&](int kq, KData& d) {
+            const int qc = kq * 16 + 8 * hi;
+            d.A = *reinterpret_cast<const uint4*>(dyrow + qc);
 #pragma unroll
             for (int tr = 0; tr < TRB; ++tr) {
-                const uint16_t* xr = xrows[tr];
-                Pack8 lo, hh;
-                lo.v = *reinterpret_cast<const uint4*>(xr + qc);
-                hh.v = *reinterpret_cast<const uint4*>(xr + qc + 8);
-                const uint32_t d[8] = {lo.d[0], lo.d[1], lo.d[2], lo.d[3],
-                                       hh.d[0], hh.d[1], hh.d[2], hh.d[3]};
-#pragma unroll
-                for (int s = 0; s < SS; ++s) {
-                    Pack8 B;
-                    B.v = (s == 0) ? window8<0>(d) : (s == 1) ? window8<1>(d) : (s == 2) ? window8<2>(d)
-                        : (s == 3) ? window8<3>(d) : (s == 4) ? window8<4>(d) : (s == 5) ? window8<5>(d)
-                        : window8<6>(d);
-                    acc[tr][s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.b, B.b, acc[tr][s], 0, 0, 0);
+                const uint4 lo = *reinterpret_cast<const uint4*>(xrows[tr] + qc);
+                d.x[tr][0] = lo.x; d.x[tr][1] = lo.y; d.x[tr][2] = lo.z; d.x[tr][3] = lo.w;
+                if constexpr (XH == 2) {
+                    const uint2 h = *reinterpret_cast<const uint2*>(xrows[tr] + qc + 8);
+                    d.x[tr][4] = h.x; d.x[tr][5] = h.y;
+                } else {
+                    const uint4 h = *reinterpret_cast<const uint4*>(xrows[tr] + qc + 8);
+                    d.x[tr][4] = h.x; d.x[tr][5] = h.y; d.x[tr][6] = h.z; d.x[tr][7] = h.w;
                 }
             }
-        }
-        if (i + 1 < nrows) {   // step i+1's data, loaded during step i-1
-            store_x(i + nTR, nxt);
-            store_dy(i + 1, nxt);
-        }
+        };
+        // MFMAs of one k-step; `mid` runs after the first `at` of them, so that
+        // its VALU and memory work issues while the matrix cores are busy
+        auto mfmas_k = [&](const KData& d, auto at, auto&& mid) {
+            Pack8 A;
+            A.v = d.A;
+            constexpr int AT0 = decltype(at)::value;
+            constexpr int AT = AT0 < 0 ? -1 : (AT0 < TRB * SS ? AT0 : TRB * SS - 1);
+            static_for<0, TRB * SS>([&](auto fc) {
+                constexpr int f = decltype(fc)::value, tr = f / SS, s = f % SS;
+                if constexpr (f == AT) mid();
+                Pack8 B;
+                uint32_t* o = B.d;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if constexpr ((s & 1) == 0)
+                        o[j] = d.x[tr][s / 2 + j];
+                    else
+                        o[j] = __builtin_amdgcn_alignbyte(d.x[tr][s / 2 + j + 1], d.x[tr][s / 2 + j], 2);
+                }
+                floatx16& ac = acc[tr][s];
+                const bf16x8 av = A.b, bv = B.b;
+                // B is written by VALU (byte-align or register copies) just before
+                if constexpr (s == 0)
+                    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(ac) : "v"(av), "v"(bv));
+                else
+                    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                                 : "+a"(ac) : "v"(av), "v"(bv));
+            });
+        };
+        constexpr int NK = kBQ / 16;
+        KData kd[2];
+        read_k(0, kd[0]);
+        static_for<0, NK>([&](auto kc) {
+            constexpr int kq = decltype(kc)::value;
+            if constexpr (kq + 1 < NK) read_k(kq + 1, kd[(kq + 1) & 1]);
+            if constexpr (kq == 0) {
+                // step i+2's data: two steps of MFMAs to arrive
+                mfmas_k(kd[0], std::integral_constant<int, 1>{}, [&] {
+                    load_x(i + 1 + nTR, cur);
+                    load_dy(i + 2, cur);
+                });
+            } else if constexpr (kq == NK - 1) {
+                // step i+1's data (loaded during step i-1) into slots this step does not read
+                mfmas_k(kd[kq & 1], std::integral_constant<int, 1>{}, [&] {
+                    store_x(i + nTR, nxt);
+                    store_dy(i + 1, nxt);
+                });
+            } else {
+                mfmas_k(kd[kq & 1], std::integral_constant<int, -1>{}, [] {});
+            }
+        });
         __syncthreads();
     };
-    for (int i = 0; i < nrows; i += 2) {
+    int i = 0;
+    for (; i + 1 < nrows; i += 2) {
         step(i, bufA, bufB);
-        if (i + 1 < nrows) step(i + 1, bufB, bufA);
+        step(i + 1, bufB, bufA);
     }
+    if (i < nrows) step(i, bufA, bufB);
+#pragma unroll
+    for (int i = 0; i < TRB; ++i)
+#pragma unroll
+        for (int j = 0; j < SS; ++j) mfma_drain(acc[i][j]);
 
     // partial in fragment order: [chunk][gy][gz][wave][tr][s][16][64]
     float* part = a.part + int64_t(blockIdx.x) * a.F +
