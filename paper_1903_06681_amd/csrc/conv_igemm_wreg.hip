@@ -132,55 +132,42 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     constexpr int T = TR * TS;
     constexpr int RL = CIN * T;                                    // row length
     constexpr int PW = ((RL * 2 + 239) / 256 * 256 + 16) / 2;      // 2*PW = 16 (mod 256)
+    const int nO = min(OBT, a.Cout - o0);                         // valid output channels here
     uint16_t* Wl = lds;
     {
         const uint16_t* w = static_cast<const uint16_t*>(a.w);
-        // Every workgroup reads the same block of w at the same moment: start
-        // each one at its own offset so that the requests spread out.
-        const unsigned rot0 = blockIdx.x * 149u + blockIdx.y * 31u;
         if (a.wvec && a.wmode == 0) {
             // rows o0 .. o0+OBT-1 of w are consecutive: 16-byte chunks straight to
-            // LDS, all of a thread's loads in flight at once
+            // LDS, all of a thread's loads in flight at once (chunks of rows
+            // past Cout re-read the last valid chunk)
             constexpr int CPR = RL / 8, NCH = OBT * CPR, NB = (NCH + kWThreads - 1) / kWThreads;
-            const int rot = int(rot0 % unsigned(NCH));
+            const int last = nO * CPR - 1;
+            const uint4* src = reinterpret_cast<const uint4*>(w + int64_t(o0) * RL);
             uint4 buf[NB];
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                int v = min(b * kWThreads + tid, NCH - 1) + rot;
-                v = v >= NCH ? v - NCH : v;
-                const int o = min(o0 + v / CPR, a.Cout - 1), cc = v % CPR;
-                buf[b] = *reinterpret_cast<const uint4*>(w + int64_t(o) * RL + cc * 8);
-            }
+            for (int b = 0; b < NB; ++b) buf[b] = src[min(b * kWThreads + tid, last)];
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
-                int v = b * kWThreads + tid;
-                if (v < NCH) {
-                    v += rot;
-                    v = v >= NCH ? v - NCH : v;
-                    *reinterpret_cast<uint4*>(Wl + (v / CPR) * PW + (v % CPR) * 8) = buf[b];
-                }
+                const int v = b * kWThreads + tid;
+                if (v < NCH) *reinterpret_cast<uint4*>(Wl + (v / CPR) * PW + (v % CPR) * 8) = buf[b];
             }
         } else if (a.wvec) {
             // row ci of w holds (o, t) of this block as OBT*T consecutive elements
             constexpr int CPR = OBT * T / 8, NCH = CIN * CPR, NB = (NCH + kWThreads - 1) / kWThreads;
             const int64_t rs = int64_t(a.Cout) * T;                 // w row stride
             const int64_t last = int64_t(a.Cout) * T - 8;           // last chunk start in a row
-            const int rot = int(rot0 % unsigned(NCH));
             uint4 buf[NB];
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
-                int v = min(b * kWThreads + tid, NCH - 1) + rot;
-                v = v >= NCH ? v - NCH : v;
+                const int v = min(b * kWThreads + tid, NCH - 1);
                 const int ci = v / CPR, cc = v % CPR;
                 const int64_t col = min(int64_t(o0) * T + cc * 8, last);
                 buf[b] = *reinterpret_cast<const uint4*>(w + ci * rs + col);
             }
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
-                int v = b * kWThreads + tid;
+                const int v = b * kWThreads + tid;
                 if (v < NCH) {
-                    v += rot;
-                    v = v >= NCH ? v - NCH : v;
                     const int ci = v / CPR, e0 = (v % CPR) * 8;
                     Pack8 pk;
                     pk.v = buf[b];
