@@ -152,29 +152,34 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 if (v < NCH) *reinterpret_cast<uint4*>(Wl + (v / CPR) * PW + (v % CPR) * 8) = buf[b];
             }
         } else if (a.wvec) {
-            // row ci of w holds (o, t) of this block as OBT*T consecutive elements
-            constexpr int CPR = OBT * T / 8, NCH = CIN * CPR, NB = (NCH + kWThreads - 1) / kWThreads;
+            // row ci of w holds (o, t) of this block as OBT*T consecutive
+            // elements.  Each thread keeps one 16-byte chunk position c of the
+            // rows and walks rows ci = r0, r0 + TPR, ...: the LDS positions of
+            // its chunk's 8 elements are then per-thread constants plus a
+            // compile-time row offset.
+            constexpr int CPR = OBT * T / 8, TPR = kWThreads / CPR, NR = (CIN + TPR - 1) / TPR;
             const int64_t rs = int64_t(a.Cout) * T;                 // w row stride
             const int64_t last = int64_t(a.Cout) * T - 8;           // last chunk start in a row
-            uint4 buf[NB];
+            if (tid < TPR * CPR) {
+                const int c = tid % CPR, r0 = tid / CPR;
+                const uint16_t* src = w + min(int64_t(o0) * T + c * 8, last);
+                uint4 buf[NR];
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int v = min(b * kWThreads + tid, NCH - 1);
-                const int ci = v / CPR, cc = v % CPR;
-                const int64_t col = min(int64_t(o0) * T + cc * 8, last);
-                buf[b] = *reinterpret_cast<const uint4*>(w + ci * rs + col);
-            }
+                for (int r = 0; r < NR; ++r)
+                    buf[r] = *reinterpret_cast<const uint4*>(src + min(r0 + r * TPR, CIN - 1) * rs);
+                uint16_t* dst[8];
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int v = b * kWThreads + tid;
-                if (v < NCH) {
-                    const int ci = v / CPR, e0 = (v % CPR) * 8;
-                    Pack8 pk;
-                    pk.v = buf[b];
+                for (int j = 0; j < 8; ++j) {
+                    const int e = c * 8 + j, o = e / T, t = e % T;
+                    dst[j] = Wl + o * PW + r0 * T + (T - 1 - t);
+                }
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int o = (e0 + j) / T, t = (e0 + j) % T;
-                        Wl[o * PW + ci * T + (T - 1 - t)] = pk.h[j];
+                for (int r = 0; r < NR; ++r) {
+                    if (r0 + r * TPR < CIN) {
+                        Pack8 pk;
+                        pk.v = buf[r];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) dst[j][r * TPR * T] = pk.h[j];
                     }
                 }
             }
