@@ -62,6 +62,20 @@ def algorithmic(L):
     }
 
 
+def halo_payload_bytes(L):
+    """Bytes a pack of the whole grid sends: the real halo regions of every tile."""
+    e = 2 if L.dtype == "bf16" else 4
+    h, tot = L.halo, 0
+    for ti in range(L.P):
+        for tj in range(L.Q):
+            for di in (-1, 0, 1):
+                for dj in (-1, 0, 1):
+                    if (di, dj) == (0, 0) or not (0 <= ti + di < L.P and 0 <= tj + dj < L.Q):
+                        continue
+                    tot += L.N * L.C * (h if di else L.Ht) * (h if dj else L.Wt) * e
+    return tot
+
+
 def source_digest():
     """sha256 over the library's kernel and host sources: changes with any kernel change."""
     import hashlib
@@ -177,7 +191,8 @@ def main():
     ap.add_argument("--tile", type=int, default=None, help="tile index (default: an interior tile)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=24.0)
-    ap.add_argument("--cold", action="store_true", help="also time steps after a cache flush")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold timings (each step or pass after a 512 MB cache flush)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB a few times (the known-size "
                          "kernel against which HBM byte counters are scaled) and exit")
@@ -214,7 +229,6 @@ def main():
     sx_all = torch.empty((nt, max(dc.halo_elems(p, X), 1)), dtype=tdt, device=dev)
     dc.halo_pack(p, dc.DC_ALL_TILES, X, xt, sx_all)
     xp = xt[tile].clone()
-    del xt
     dyt = H.alloc_tiles(p, DY, nt, L.dtype)
     H.scatter_interiors(dyt, H.to_device(dy, L.dtype), p, DY)
     sy_all = torch.empty((nt, max(dc.halo_elems(p, DY), 1)), dtype=tdt, device=dev)
@@ -340,18 +354,59 @@ def main():
         "setup_s": round(t_setup, 1),
     }
 
-    if args.cold:
+    # halo pack / unpack of the whole grid in one launch each (all tiles)
+    payload = halo_payload_bytes(L)
+    sx_grid = torch.empty((nt, max(dc.halo_elems(p, X), 1)), dtype=tdt, device=dev)
+    grid_calls = {"pack_x_all_tiles": lambda: dc.halo_pack(p, dc.DC_ALL_TILES, X, xt, sx_grid, sh),
+                  "unpack_x_all_tiles": lambda: dc.halo_unpack(p, dc.DC_ALL_TILES, X, sx_grid, xt, sh)}
+    grid = {}
+    for n, c in grid_calls.items():
+        c()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            c()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        warm = e0.elapsed_time(e1) / args.steps
+        grid[n] = {"payload_bytes": payload, "ms": round(warm, 5),
+                   "useful_GB/s": round(2 * payload / (warm * 1e-3) / 1e9, 1)}
+    out["halo_all_tiles"] = grid
+
+    if not args.no_cold:
+        # Cold timings: a 512 MB write (more than the 256 MB Infinity Cache and
+        # the L2s) before each timed interval, outside it.  A single launch
+        # between two events also pays one dispatch, so cold pass times sit a
+        # few microseconds above the back-to-back ones.
         flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
-        cold = []
-        for _ in range(min(args.steps, 10)):
-            flush.zero_()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            step()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            cold.append(e0.elapsed_time(e1))
-        out["cold_ms_per_step"] = round(float(np.mean(cold)), 5)
+
+        def cold_ms(fn, reps):
+            ts = []
+            for _ in range(reps):
+                flush.zero_()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            return {"mean": round(float(np.mean(ts)), 5), "std": round(float(np.std(ts)), 5),
+                    "min": round(float(np.min(ts)), 5), "runs": reps}
+
+        reps = max(3, min(args.steps, 10))
+        out["cold_step_ms"] = cold_ms(step, reps)
+        for n, c in zip(names, calls):
+            cm = cold_ms(c, reps)
+            passes[n]["cold_ms"] = cm
+            if alg[n]["flops"]:
+                passes[n]["cold_TFLOP/s"] = round(alg[n]["flops"] / (cm["mean"] * 1e-3) / 1e12, 2)
+            passes[n]["cold_GB/s"] = round(alg[n]["bytes"] / (cm["mean"] * 1e-3) / 1e9, 1)
+        for n, c in grid_calls.items():
+            cm = cold_ms(c, reps)
+            grid[n]["cold_ms"] = cm
+            grid[n]["cold_useful_GB/s"] = round(2 * payload / (cm["mean"] * 1e-3) / 1e9, 1)
+
         del flush
 
     if not args.no_cpu_baseline:
