@@ -73,6 +73,13 @@ SMALL = {
     "s2_f32": Layer("s2_f32", 2, 5, 6, 23, 23, 3, 3, 2, 1, 1, 1, 1, "f32", "uniform", 80),
     "s2k7_f32": Layer("s2k7_f32", 2, 3, 8, 30, 30, 7, 7, 2, 3, 1, 1, 3, "f32", "uniform", 81),
     "wide_bf16": Layer("wide_bf16", 1, 72, 80, 20, 150, 3, 3, 1, 1, 1, 2, 1, "bf16", "uniform", 82),
+    # channel counts that leave a partial 64-wide output block in the
+    # register-resident-weight kernels and a partial filter block in the
+    # weight-gradient strip kernel
+    "k80_bf16": Layer("k80_bf16", 2, 64, 80, 40, 40, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 83),
+    "c32k48_bf16": Layer("c32k48_bf16", 2, 32, 48, 36, 36, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 84),
+    "k1_48_bf16": Layer("k1_48_bf16", 2, 64, 48, 24, 24, 1, 1, 1, 0, 2, 2, 0, "bf16", "uniform", 85),
+    "c48k64_bf16": Layer("c48k64_bf16", 2, 48, 64, 36, 36, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 86),
 }
 
 
@@ -120,7 +127,8 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
     _check("dw", dwg, dwr, L.dtype)
 
 
-@pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s"])
+@pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
+                                  "k80_bf16", "c48k64_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
