@@ -37,7 +37,7 @@ typedef enum {
     DC_ERR_SHAPE       = -2,  /* a size is non-positive, or sizes are inconsistent */
     DC_ERR_DTYPE       = -3,  /* dtype is not DC_F32 / DC_BF16 */
     DC_ERR_HALO        = -4,  /* halo narrower than the pass needs, or wider than a tile */
-    DC_ERR_UNSUPPORTED = -5,  /* uneven tiles, decomposed stride > 1, non-"same" decomposed output */
+    DC_ERR_UNSUPPORTED = -5,  /* uneven tiles, or a decomposed output grid not aligned with the input grid */
     DC_ERR_WORKSPACE   = -6,  /* workspace NULL or smaller than dc_bwd_filter_workspace_bytes() */
     DC_ERR_ALIGN       = -7,  /* a device pointer is not 16-byte aligned */
     DC_ERR_HIP         = -8,  /* the HIP runtime reported an error at launch */
@@ -59,12 +59,17 @@ typedef enum { DC_X = 0, DC_DY = 1 } dc_which;       /* which tensor a tile/halo
  * distributions of H and W).  The global output is Ho x Wo with
  * Ho = (H + 2*pad - R)/stride + 1; a tile owns Hot = Ho/P by Wot = Wo/Q of it.
  * With P = Q = 1 any geometry with Ho, Wo >= 1 is accepted; with more than one
- * tile the layer must have stride 1 and "same" output (Ho = H, Wo = W).
+ * tile the output grid must line up with the input grid, Ho * stride = H and
+ * Wo * stride = W (stride 1: "same" output), and Ho % P = Wo % Q = 0, so that
+ * a tile owns exactly the outputs whose taps start in its input block.  At
+ * stride > 1 a tile may need no halo on one side (e.g. 3x3 stride 2 pad 1: x
+ * 1 below, 0 above); the one width h still serves every side.
  *
  * halo is the margin width h kept on every side of every tile (for both the x
  * and the dy tile).  It must be at least what each pass reads beyond the tile
  * (see dc_required_halo) and, with more than one tile along an axis, at most
- * the tile extent along it (halos come from the adjacent tile only).
+ * the input and the output tile extent along it (halos come from the
+ * adjacent tile only).
  */
 typedef struct {
     int32_t N, C, K;       /* samples on this GPU, input channels, filters */

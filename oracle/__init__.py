@@ -348,30 +348,36 @@ def needed_halo_dy(Ho, R, stride, pad, Ht, Hot, t0_in, t0_out):
 # Decomposed (tiled) computation, Sec. III-A
 # --------------------------------------------------------------------------
 
-def tiled_conv(x, w, dy, P, Q, h, pad):
-    """Stride-1 decomposed forward, backward-data and backward-filter over a
-    P x Q grid with halo width h >= needed.  Every tile convolves its own
-    window (pad 0); y and dx are stitched; the dw partials are summed in fp64
-    in row-major tile order.  Returns (y, dx, dw) in fp64."""
+def tiled_conv(x, w, dy, P, Q, h, pad, stride=1):
+    """Decomposed forward, backward-data and backward-filter over a P x Q grid
+    of blocked tiles with halo width h >= needed (Sec. III-A).  With stride s
+    an input tile of Ht x Wt owns the Ht/s x Wt/s output block whose taps start
+    in it.  Every tile works on its own window (owned block plus h on every
+    side, zeros outside the domain):
+      y:  Eq. (1) over the window rows from h - pad on, pad 0;
+      dx: Eq. (3) over the whole dy window, whose row 0 sits h output rows
+          above the tile, so the taps are shifted by h*s (pad + h*s);
+      dw: Eq. (2) over the dy interior and the same x rows as y.
+    y and dx are stitched; the dw partials are summed in fp64 in row-major
+    tile order.  Returns (y, dx, dw) in fp64."""
     N, C, H, W = x.shape
     K, _, R, S = w.shape
     Ht, Wt = H // P, W // Q
-    lo, hi = pad, R - 1 - pad  # rows of x each output row reaches below/above
-    y = np.zeros((N, K, H, W))
+    Hot, Wot = Ht // stride, Wt // stride
+    nr, ns = (Hot - 1) * stride + R, (Wot - 1) * stride + S   # x rows/cols one tile reads
+    y = np.zeros((N, K, Hot * P, Wot * Q))
     dx = np.zeros((N, C, H, W))
     dw = np.zeros((K, C, R, S))
     for ti in range(P):
         for tj in range(Q):
             xw = tile_window(x, P, Q, ti, tj, h)
-            dyw = tile_window(dy, P, Q, ti, tj, h)
-            xs = np.ascontiguousarray(xw[:, :, h - lo:h + Ht + hi, h - lo:h + Wt + hi])
-            yt = conv_fwd(xs, w, 1, 0)
-            # dx rows i need dy rows i+pad-r: from -(R-1-pad) to Ht-1+pad
-            dys = np.ascontiguousarray(dyw[:, :, h - hi:h + Ht + lo, h - hi:h + Wt + lo])
-            dxt = conv_bwd_data(dys, w, Ht, Wt, 1, R - 1)
-            dyo = np.ascontiguousarray(dyw[:, :, h:h + Ht, h:h + Wt])
-            dwt = conv_bwd_filter(xs, dyo, R, S, 1, 0)
-            y[:, :, ti * Ht:(ti + 1) * Ht, tj * Wt:(tj + 1) * Wt] = yt
+            dyw = tile_window(dy, P, Q, ti, tj, h)    # dy tiles are Hot x Wot, same grid
+            xs = np.ascontiguousarray(xw[:, :, h - pad:h - pad + nr, h - pad:h - pad + ns])
+            yt = conv_fwd(xs, w, stride, 0)
+            dxt = conv_bwd_data(np.ascontiguousarray(dyw), w, Ht, Wt, stride, pad + h * stride)
+            dyo = np.ascontiguousarray(dyw[:, :, h:h + Hot, h:h + Wot])
+            dwt = conv_bwd_filter(xs, dyo, R, S, stride, 0)
+            y[:, :, ti * Hot:(ti + 1) * Hot, tj * Wot:(tj + 1) * Wot] = yt
             dx[:, :, ti * Ht:(ti + 1) * Ht, tj * Wt:(tj + 1) * Wt] = dxt
             dw += dwt
     return y, dx, dw

@@ -52,9 +52,13 @@ dc_status make_geo(const dc_problem* p, Geo* g) {
     if (p->H % p->P != 0 || p->W % p->Q != 0) return DC_ERR_UNSUPPORTED;
     g->ntiles = p->P * p->Q;
     if (g->ntiles > 1) {
-        // Decomposed layers: stride 1 and "same" output, so output tiles
-        // coincide with input tiles (Sec. III-A's setting).
-        if (p->stride != 1 || g->Ho != p->H || g->Wo != p->W) return DC_ERR_UNSUPPORTED;
+        // Decomposed layers (Sec. III-A): the output grid must line up with
+        // the input grid, Ho * stride == H, so that the Ht/stride x Wt/stride
+        // output block of a tile is exactly the outputs whose taps start in
+        // it; and the output tiles must divide evenly too.
+        if (int64_t(g->Ho) * p->stride != p->H || int64_t(g->Wo) * p->stride != p->W)
+            return DC_ERR_UNSUPPORTED;
+        if (g->Ho % p->P != 0 || g->Wo % p->Q != 0) return DC_ERR_UNSUPPORTED;
     }
     g->Ht = p->H / p->P; g->Wt = p->W / p->Q;
     g->Hot = g->Ho / p->P; g->Wot = g->Wo / p->Q;
@@ -66,8 +70,9 @@ dc_status make_geo(const dc_problem* p, Geo* g) {
     int need = std::max({g->need_x_lo_r, g->need_x_hi_r, g->need_x_lo_s, g->need_x_hi_s,
                          g->need_dy_lo_r, g->need_dy_hi_r, g->need_dy_lo_s, g->need_dy_hi_s});
     if (g->h < need) return DC_ERR_HALO;
-    // halos come from the adjacent tile only
-    if ((p->P > 1 && g->h > g->Ht) || (p->Q > 1 && g->h > g->Wt)) return DC_ERR_HALO;
+    // halos come from the adjacent tile only (for x and for dy tiles)
+    if ((p->P > 1 && (g->h > g->Ht || g->h > g->Hot)) || (p->Q > 1 && (g->h > g->Wt || g->h > g->Wot)))
+        return DC_ERR_HALO;
 
     const int align = 16 / g->esize;
     g->x_rows = g->Ht + 2 * g->h;  g->x_cols = g->Wt + 2 * g->h;

@@ -80,6 +80,11 @@ SMALL = {
     "c32k48_bf16": Layer("c32k48_bf16", 2, 32, 48, 36, 36, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 84),
     "k1_48_bf16": Layer("k1_48_bf16", 2, 64, 48, 24, 24, 1, 1, 1, 0, 2, 2, 0, "bf16", "uniform", 85),
     "c48k64_bf16": Layer("c48k64_bf16", 2, 48, 64, 36, 36, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 86),
+    # decomposed stride 2 (Sec. III-A): output tiles of Ht/2 x Wt/2, one-sided halos
+    "s2dec_f32": Layer("s2dec_f32", 2, 5, 6, 32, 24, 3, 3, 2, 1, 2, 2, 1, "f32", "uniform", 87),
+    "s2dec_bf16": Layer("s2dec_bf16", 2, 16, 32, 32, 32, 3, 3, 2, 1, 2, 2, 1, "bf16", "uniform", 88),
+    "s2k7dec_f32": Layer("s2k7dec_f32", 1, 3, 8, 32, 32, 7, 7, 2, 3, 2, 2, 3, "f32", "uniform", 89),
+    "s2k1dec_bf16": Layer("s2k1dec_bf16", 2, 32, 48, 32, 32, 1, 1, 2, 0, 2, 2, 0, "bf16", "uniform", 90),
 }
 
 
@@ -128,7 +133,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
-                                  "k80_bf16", "c48k64_bf16"])
+                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
@@ -141,7 +146,7 @@ def test_integer_inputs_are_bit_exact(name):
     _check("dw", dwg, dwr, L.dtype, exact=True)
 
 
-@pytest.mark.parametrize("name", ["c2", "odd_bf16", "c5b_s"])
+@pytest.mark.parametrize("name", ["c2", "odd_bf16", "c5b_s", "s2k7dec_f32"])
 def test_single_tile_calls_match_all_tiles(name):
     """Per-tile pack -> emulated exchange (region copies) -> unpack -> passes
     equals the all-tiles launch bit for bit, and accumulate=1 sums the tiles."""
@@ -305,7 +310,7 @@ def _sample_idx(rng, shape, region, n_rand, edges=True):
 
 
 FULL = [("c5a", 5), ("c5a", 0), ("c5b", 5), ("c5b", 0), ("c4", 5), ("c4", 0),
-        ("c3a", 0), ("c3b", 0), ("c3c", 0)]
+        ("c3a", 0), ("c3b", 0), ("c3c", 0), ("c3a_2x2", 3), ("c3a_2x2", 0), ("c4s2", 5), ("c4s2", 0)]
 
 
 @pytest.mark.parametrize("name,tile", FULL)
@@ -366,10 +371,11 @@ def test_full_size_single_tile_sampled(name, tile):
     if L.P * L.Q == 1:
         xs, dys, pad = x, dy, L.pad
     else:
-        lo, hi = L.pad, L.R - 1 - L.pad
+        # the x rows/cols the tile's outputs reach: from -pad, (Hot-1)*stride + R of them
+        nr, ns = (L.Hot - 1) * L.stride + L.R, (L.Wot - 1) * L.stride + L.S
         win = orc.tile_window(x, L.P, L.Q, ti, tj, L.halo)
         h = L.halo
-        xs = np.ascontiguousarray(win[:, :, h - lo:h + L.Ht + hi, h - lo:h + L.Wt + hi])
+        xs = np.ascontiguousarray(win[:, :, h - L.pad:h - L.pad + nr, h - L.pad:h - L.pad + ns])
         dys = np.ascontiguousarray(dy[:, :, ti * L.Hot:(ti + 1) * L.Hot, tj * L.Wot:(tj + 1) * L.Wot])
         pad = 0
     n_dw = min(256, dw.size)

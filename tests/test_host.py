@@ -46,7 +46,12 @@ def test_every_declared_function_is_exported():
     ({"R": 5, "S": 5, "pad": 2}, -4),        # needs 2, has 1
     ({"halo": 17}, -4),                      # wider than a 16-wide tile
     ({"H": 33}, -5),                         # uneven tiles
-    ({"stride": 2}, -5),                     # decomposed stride 2
+    ({"stride": 2}, 0),                      # decomposed stride 2: 16x16 output tiles of 8
+    ({"stride": 2, "H": 36, "W": 36, "P": 4, "Q": 4}, -5),   # output 18 not divisible by 4
+    ({"stride": 2, "pad": 0, "halo": 2}, -5),    # output 15 * 2 != 32: grids do not line up
+    ({"stride": 2, "R": 7, "S": 7, "pad": 3, "halo": 2}, -4),   # x needs 3 below
+    ({"stride": 2, "R": 7, "S": 7, "pad": 3, "halo": 3}, 0),
+    ({"stride": 2, "H": 16, "W": 16, "P": 4, "Q": 4, "halo": 3, "R": 7, "S": 7, "pad": 3}, -4),  # dy tile 2 < h
     ({"pad": 0, "halo": 2}, -5),             # decomposed, output not "same"
     ({"H": 2, "W": 2, "P": 1, "Q": 1, "pad": 0}, -2),  # empty output
     ({"P": 1, "Q": 1, "R": 1, "S": 1, "pad": 0, "halo": 0}, 0),
@@ -72,6 +77,7 @@ def test_all_workloads_validate():
 
 @pytest.mark.parametrize("R,stride,pad,H,P", [
     (3, 1, 1, 32, 2), (5, 1, 2, 40, 4), (1, 1, 0, 16, 2), (7, 2, 3, 224, 1), (3, 2, 1, 16, 1),
+    (3, 2, 1, 32, 2), (7, 2, 3, 64, 4), (1, 2, 0, 16, 2), (5, 2, 2, 24, 3),
     (3, 1, 0, 12, 1), (4, 1, 1, 20, 1), (1, 2, 0, 14, 1), (5, 2, 1, 21, 1), (3, 3, 2, 17, 1),
 ])
 def test_required_halo_matches_brute_force(R, stride, pad, H, P):

@@ -279,3 +279,35 @@ def test_decomposed_equals_undecomposed(P, Q, h, R, pad, kind):
     else:
         ulp = np.abs(np.spacing(dw0))
         assert np.all(np.abs(dw0.astype(np.float64) - dw1) <= ulp)
+
+
+
+@pytest.mark.parametrize("P,Q,h,R,pad,stride,kind", [
+    (2, 2, 1, 3, 1, 2, "real"), (2, 2, 1, 3, 1, 2, "int"), (4, 2, 3, 7, 3, 2, "real"),
+    (2, 2, 3, 7, 3, 2, "int"), (2, 2, 0, 1, 0, 2, "real"), (2, 2, 1, 1, 0, 2, "real"),
+    (3, 2, 2, 5, 2, 2, "real"), (2, 2, 1, 3, 1, 3, "int"),
+])
+def test_decomposed_stride_equals_undecomposed(P, Q, h, R, pad, stride, kind):
+    """Stride > 1 (Sec. III-A): an input tile of Ht x Wt owns the Ht/s x Wt/s
+    output block.  The decomposed passes replicate the undecomposed ones: y and
+    dx bit for bit, dw within one fp32 ulp (bit for bit on integers)."""
+    rng = np.random.default_rng(P * 1000 + Q * 100 + h * 10 + R + 7 * stride)
+    N, C, K = 2, 3, 4
+    H, W = 4 * stride * P, 3 * stride * Q
+    assert orc.out_size(H, R, stride, pad) * stride == H   # output tiles align with input tiles
+    x = _rand(rng, (N, C, H, W), kind)
+    w = _rand(rng, (K, C, R, R), kind)
+    Ho, Wo = H // stride, W // stride
+    dy = _rand(rng, (N, K, Ho, Wo), kind)
+    y0 = orc.round_f32(orc.conv_fwd(x, w, stride, pad))
+    dx0 = orc.round_f32(orc.conv_bwd_data(dy, w, H, W, stride, pad))
+    dw0 = orc.round_f32(orc.conv_bwd_filter(x, dy, R, R, stride, pad))
+    y1, dx1, dw1 = (orc.round_f32(a) for a in orc.tiled_conv(x, w, dy, P, Q, h, pad, stride))
+    assert np.array_equal(y0, y1)
+    assert np.array_equal(dx0, dx1)
+    if kind == "int":
+        assert np.array_equal(dw0, dw1)
+    else:
+        ulp = np.abs(np.spacing(dw0))
+        assert np.all(np.abs(dw0.astype(np.float64) - dw1) <= ulp)
+

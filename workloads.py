@@ -100,6 +100,15 @@ LAYERS = {
     "c5b": Layer("c5b", 4, 32, 32, 1024, 1024, 5, 5, 1, 2, 4, 4, 2, "bf16", "uniform", 1004, 1,
                  tiles=(5, 0),
                  desc="5x5 s1 p2, C=K=32, N=4, 256x256 tile of 1024x1024 (4x4 grid), h=2, bf16"),
+    # decomposed stride-2 layers (Sec. III-A: one-sided halos at stride > 1)
+    "c3a_2x2": Layer("c3a_2x2", 32, 3, 64, 224, 224, 7, 7, 2, 3, 2, 2, 3, "bf16", "uniform", 1002, 3,
+                     tiles=(3, 0),
+                     desc="ResNet-50 conv1 7x7 s2 p3, C=3->K=64, 224x224 on a 2x2 grid (112x112 tiles, "
+                          "56x56 outputs), h=3, N=32, bf16"),
+    "c4s2": Layer("c4s2", 1, 32, 32, 2048, 2048, 3, 3, 2, 1, 4, 4, 1, "f32", "normal", 1003, 1,
+                  tiles=(5, 0),
+                  desc="mesh-2K-like stride-2 3x3 p1 block entry, C=K=32, 512x512 tile of 2048x2048 "
+                       "(4x4 grid, 256x256 outputs), h=1, fp32"),
 }
 
 # The layer the benchmark times: the largest conv tile by flops and bytes.
