@@ -39,6 +39,7 @@ namespace dc {
 static constexpr int kThreads = 256;
 static constexpr int kBQ = 64;          // output columns staged per step
 static constexpr int kTargetWGs = 256;  // workgroups aimed for per launch (one per CU)
+static constexpr int kDepth = 2;        // strip kernel: steps between a row's loads and its use
 
 
 // ---------------------------------------------------------------- planning
@@ -67,20 +68,34 @@ struct Plan {
     int frag;
 };
 
+// tap-split kernel: square filters whose R*S taps spread over four waves fit
+// the accumulators (at most 14 tiles of 32x32 per wave)
+static bool taps_filter(int R, int S) { return R == S && R >= 2 && R <= 7; }
+
 static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, int stride,
                       int Hot, int Wot, int base_c, Plan* pl) {
     std::memset(pl, 0, sizeof(*pl));
     const bool xcol_aligned = base_c % 8 == 0;   // strip staging reads whole 16-byte x chunks
     if (dtype == 1 && stride == 1 && S <= 7 && xcol_aligned) {
-        pl->kind = WGRAD_STRIP_BF16;
-        // filter rows per workgroup: the largest divisor of R that fits the
-        // accumulators (rows x S <= 9 tiles of 32x32), so every group is full
-        int trb = 1;
-        for (int d = 1; d <= std::min(bf16_trb(S), R); ++d)
-            if (R % d == 0) trb = d;
-        pl->TRB = trb;
-        pl->gy = (R + pl->TRB - 1) / pl->TRB;
-        pl->gz = ((K + 63) / 64) * ((C + 63) / 64);
+        if (C <= 32 && K <= 32 && taps_filter(R, S)) {
+            // one 32x32 block, every tap in one row group: x and dy are read once
+            pl->kind = WGRAD_TAPS_BF16;
+            pl->TRB = R;
+            pl->gy = 1;
+            pl->gz = 1;
+            pl->frag = 2;
+        } else {
+            pl->kind = WGRAD_STRIP_BF16;
+            // filter rows per workgroup: the largest divisor of R that fits the
+            // accumulators (rows x S <= 9 tiles of 32x32), so every group is full
+            int trb = 1;
+            for (int d = 1; d <= std::min(bf16_trb(S), R); ++d)
+                if (R % d == 0) trb = d;
+            pl->TRB = trb;
+            pl->gy = (R + pl->TRB - 1) / pl->TRB;
+            pl->gz = ((K + 63) / 64) * ((C + 63) / 64);
+            pl->frag = 1;
+        }
         pl->nqb = (Wot + kBQ - 1) / kBQ;
         const int strips = ntiles * N * pl->nqb;
         const int want = std::max(1, kTargetWGs / (pl->gy * pl->gz));
@@ -88,8 +103,7 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
         pl->rows_per_seg = (Hot + nseg - 1) / nseg;
         pl->nseg = (Hot + pl->rows_per_seg - 1) / pl->rows_per_seg;
         pl->nchunks = strips * pl->nseg;
-        pl->F = int64_t(pl->gy) * pl->gz * 4 * pl->TRB * S * 1024;
-        pl->frag = 1;
+        pl->F = int64_t(pl->gy) * pl->gz * (pl->frag == 1 ? 4 : 1) * pl->TRB * S * 1024;
         return true;
     }
     if (dtype == 1) {
@@ -131,8 +145,9 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
     a.chunks_per_tile = pl.chunks_per_tile; a.rows_per_chunk = pl.rows_per_chunk;
     a.nqb = pl.nqb; a.nseg = pl.nseg; a.rows_per_seg = pl.rows_per_seg;
     a.F = pl.F; a.frag = pl.frag;
-    if (a.kind == WGRAD_STRIP_BF16) {
-        a.lds_bytes = ((a.TRB + 1) * 64 * kXP + 2 * 64 * kXP) * 2;
+    if (a.kind == WGRAD_STRIP_BF16 || a.kind == WGRAD_TAPS_BF16) {
+        const int cb = a.kind == WGRAD_STRIP_BF16 ? 64 : 32;
+        a.lds_bytes = ((a.TRB + 1) * cb * kXP + 2 * cb * kXP) * 2;
     } else if (a.kind == WGRAD_ROWS_BF16) {
         const int plane = odd16(a.TRB * bf16_xwp(a.istr, a.S));
         a.lds_bytes = (64 * kDyP + 64 * plane) * 2;
@@ -147,12 +162,29 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
 
 // ---------------------------------------------------------------- strip kernel (bf16)
 
-template <int SS, int TRB>
-__global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a) {
-    extern __shared__ __align__(16) unsigned char smem[];
+// Two ways to share a workgroup's block among its four waves:
+//  * kBlock64: 64 filters x 64 channels; wave = (filter half, channel half),
+//    each wave accumulates its 32 x 32 block at every tap of the row group;
+//  * kTapSplit: one 32 x 32 block (small channel counts); the row group's
+//    taps (row-major) are dealt to the waves in four contiguous runs, so a
+//    wave reads only the x rows its taps touch.
+enum StripMode { kBlock64 = 0, kTapSplit = 1 };
+
+template <int MODE, int NT>
+struct TapRange {   // taps [first(W), first(W) + count(W)) of wave W
+    static constexpr int first(int W) { return MODE == kBlock64 ? 0 : W * (NT / 4) + (W < NT % 4 ? W : NT % 4); }
+    static constexpr int count(int W) { return MODE == kBlock64 ? NT : NT / 4 + (W < NT % 4 ? 1 : 0); }
+};
+
+template <int SS, int TRB, int MODE, int W>
+__device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* smem) {
+    constexpr int CB = MODE == kBlock64 ? 64 : 32;          // channels / filters staged
     constexpr int NR = TRB + 1;                             // x ring slots
-    uint16_t* xring = reinterpret_cast<uint16_t*>(smem);    // [NR][64 ci][kXP]
-    uint16_t* dyb = xring + NR * 64 * kXP;                  // [2][64 o][kXP]
+    uint16_t* xring = reinterpret_cast<uint16_t*>(smem);    // [NR][CB ci][kXP]
+    uint16_t* dyb = xring + NR * CB * kXP;                  // [2][CB o][kXP]
+    constexpr int NT = TRB * SS;                            // taps of the row group
+    constexpr int FST = TapRange<MODE, NT>::first(W), FCNT = TapRange<MODE, NT>::count(W);
+    constexpr int RLO = FST / SS, NRW = (FST + FCNT - 1) / SS - RLO + 1;   // x rows this wave reads
 
     int c = blockIdx.x;
     const int seg = c % a.nseg; c /= a.nseg;
@@ -164,12 +196,12 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
     const int q0 = qb * kBQ;
     const int r0 = blockIdx.y * TRB;
     constexpr int nTR = TRB;                      // the plan makes every row group full
-    const int ncsb = (a.C + 63) / 64;
-    const int o0 = (blockIdx.z / ncsb) * 64, c0 = (blockIdx.z % ncsb) * 64;
+    const int ncsb = (a.C + CB - 1) / CB;
+    const int o0 = (blockIdx.z / ncsb) * CB, c0 = (blockIdx.z % ncsb) * CB;
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int l32 = lane & 31, hi = lane >> 5;
-    const int ow = wave & 1, cw = wave >> 1;
+    const int ow = MODE == kBlock64 ? wave & 1 : 0, cw = MODE == kBlock64 ? wave >> 1 : 0;
 
     const uint16_t* xt = static_cast<const uint16_t*>(a.x) + tile * a.x_tile +
                          int64_t(n) * a.C * a.x_rows * a.x_pitch;
@@ -184,20 +216,21 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
     const int xrow0 = p0 + a.base_r + r0;          // x row of ring row 0
     const int dysh = dyg0 & 7, dya0 = dyg0 - dysh;
 
-    // staging units: x row = 64 channels x 9 groups of 8; dy row = 64 filters x 8 groups
-    constexpr int XU = 64 * 9, DU = 64 * 8;
+    // staging units: x row = CB channels x 9 groups of 8; dy row = CB filters x 8 groups
+    constexpr int XU = CB * 9, DU = CB * 8;
     constexpr int XPT = (XU + kThreads - 1) / kThreads, DPT = DU / kThreads;
     // Staging in two phases so that global loads overlap the MFMAs:
     // load_*() only issues unconditional 16-byte loads from clamped addresses
     // into registers; store_*() (after the next row's MFMAs) shifts the
     // misaligned dy chunks, zeroes everything outside the tile and writes LDS.
-    // Two register buffers: the data of step j (x row j+nTR-1, dy row j) is
-    // loaded at the start of step j-2 and stored to LDS at the end of step j-1.
+    // kDepth register buffers: the data of step j (x row j+nTR-1, dy row j)
+    // is loaded at the start of step j-kDepth and stored to LDS at the end of
+    // step j-1; buffer j % kDepth holds it.
     struct Regs {
         uint4 x[XPT];
         uint4 d0[DPT], d1[DPT];
     };
-    Regs bufA, bufB;
+    Regs buf[kDepth];
 
     auto load_x = [&](int m, Regs& r) {   // ring row m -> registers
         const int gr = min(max(xrow0 + m, 0), a.x_rows - 1);
@@ -211,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
         }
     };
     auto store_x = [&](int m, Regs& r) {
-        uint16_t* slot = xring + (m % NR) * 64 * kXP;
+        uint16_t* slot = xring + (m % NR) * CB * kXP;
         const int gr = xrow0 + m;
         const bool rok = gr >= 0 && gr < a.x_rows;
 #pragma unroll
@@ -237,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
         }
     };
     auto store_dy = [&](int i, Regs& r) {
-        uint16_t* slot = dyb + (i & 1) * 64 * kXP;
+        uint16_t* slot = dyb + (i & 1) * CB * kXP;
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
             const int u = tid + k * kThreads;
@@ -252,56 +285,58 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
         }
     };
 
-    // accumulators live in AGPRs (the MFMAs are written out, see mfma32x32x16);
-    // the empty statement after zeroing settles them there
-    floatx16 acc[TRB][SS];
+    // accumulators (one per tap of this wave) live in AGPRs (the MFMAs are
+    // written out, see mfma32x32x16); the empty statement after zeroing
+    // settles them there
+    floatx16 acc[FCNT];
 #pragma unroll
-    for (int i = 0; i < TRB; ++i)
+    for (int j = 0; j < FCNT; ++j) {
 #pragma unroll
-        for (int j = 0; j < SS; ++j) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-            asm volatile("s_nop 2" : "+a"(acc[i][j]));
-        }
+        for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+        asm volatile("s_nop 2" : "+a"(acc[j]));
+    }
 
     // prologue: the filter rows of the first output row and its dy row (two
-    // rows in flight at a time), then the loads of step 1 into buffer B
-    load_dy(0, bufA);
+    // rows in flight at a time), then the loads of steps 1 .. kDepth-1
+    load_dy(0, buf[0]);
     for (int m = 0; m < nTR; m += 2) {
-        load_x(m, bufA);
-        if (m + 1 < nTR) load_x(m + 1, bufB);
-        store_x(m, bufA);
-        if (m + 1 < nTR) store_x(m + 1, bufB);
+        load_x(m, buf[0]);
+        if (m + 1 < nTR) load_x(m + 1, buf[1]);
+        store_x(m, buf[0]);
+        if (m + 1 < nTR) store_x(m + 1, buf[1]);
     }
-    store_dy(0, bufA);
-    load_x(nTR, bufB);
-    load_dy(1, bufB);
+    store_dy(0, buf[0]);
+    static_for<1, kDepth>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        load_x(j + nTR - 1, buf[j]);
+        load_dy(j, buf[j]);
+    });
     __syncthreads();
 
     // One k-step = 16 pixels: the dy chunk (A) of this lane's filter row and,
-    // per filter row tr, the 8 + (SS - 1) staged x elements from which the SS
-    // shifted windows (B) are cut.  The LDS reads of k-step kq+1 are issued
-    // before the MFMAs of k-step kq.
+    // per filter row the wave's taps touch, the 8 + (SS - 1) staged x
+    // elements from which the SS shifted windows (B) are cut.  The LDS reads
+    // of k-step kq+1 are issued before the MFMAs of k-step kq.
     constexpr int XH = SS <= 5 ? 2 : 4;   // dwords read past the first 8 elements
     struct KData {
         uint4 A;
-        uint32_t x[TRB][4 + XH];
+        uint32_t x[NRW][4 + XH];
     };
     // Loads and LDS stores are unconditional (rows past the chunk are clamped
     // reads, staged into slots no later step reads): with no branches around
     // them the wait for the loads of two steps back leaves the newer ones in
     // flight.
-    auto step = [&](int i, Regs& cur, Regs& nxt) {
-        const uint16_t* dyrow = dyb + (i & 1) * 64 * kXP + (ow * 32 + l32) * kXP;
-        const uint16_t* xrows[TRB];
+    auto step = [&](int i, Regs& cur, Regs& nxt) __attribute__((always_inline)) {
+        const uint16_t* dyrow = dyb + (i & 1) * CB * kXP + (ow * 32 + l32) * kXP;
+        const uint16_t* xrows[NRW];
 #pragma unroll
-        for (int tr = 0; tr < TRB; ++tr)
-            xrows[tr] = xring + ((i + tr) % NR) * 64 * kXP + (cw * 32 + l32) * kXP;
+        for (int tr = 0; tr < NRW; ++tr)
+            xrows[tr] = xring + ((i + RLO + tr) % NR) * CB * kXP + (cw * 32 + l32) * kXP;
         auto read_k = [&](int kq, KData& d) {
             const int qc = kq * 16 + 8 * hi;
             d.A = *reinterpret_cast<const uint4*>(dyrow + qc);
 #pragma unroll
-            for (int tr = 0; tr < TRB; ++tr) {
+            for (int tr = 0; tr < NRW; ++tr) {
                 const uint4 lo = *reinterpret_cast<const uint4*>(xrows[tr] + qc);
                 d.x[tr][0] = lo.x; d.x[tr][1] = lo.y; d.x[tr][2] = lo.z; d.x[tr][3] = lo.w;
                 if constexpr (XH == 2) {
@@ -319,10 +354,11 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
             Pack8 A;
             A.v = d.A;
             constexpr int AT0 = decltype(at)::value;
-            constexpr int AT = AT0 < 0 ? -1 : (AT0 < TRB * SS ? AT0 : TRB * SS - 1);
-            static_for<0, TRB * SS>([&](auto fc) {
-                constexpr int f = decltype(fc)::value, tr = f / SS, s = f % SS;
-                if constexpr (f == AT) mid();
+            constexpr int AT = AT0 < 0 ? -1 : (AT0 < FCNT ? AT0 : FCNT - 1);
+            static_for<0, FCNT>([&](auto jc) {
+                constexpr int j = decltype(jc)::value, f = FST + j;
+                constexpr int tr = f / SS - RLO, s = f % SS;
+                if constexpr (j == AT) mid();
                 Pack8 B;
                 uint32_t* o = B.d;
 #pragma unroll
@@ -332,7 +368,7 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
                     else
                         o[j] = __builtin_amdgcn_alignbyte(d.x[tr][s / 2 + j + 1], d.x[tr][s / 2 + j], 2);
                 }
-                floatx16& ac = acc[tr][s];
+                floatx16& ac = acc[j];
                 const bf16x8 av = A.b, bv = B.b;
                 // B is written by VALU (byte-align or register copies) just before
                 if constexpr (s == 0)
@@ -349,10 +385,10 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
             constexpr int kq = decltype(kc)::value;
             if constexpr (kq + 1 < NK) read_k(kq + 1, kd[(kq + 1) & 1]);
             if constexpr (kq == 0) {
-                // step i+2's data: two steps of MFMAs to arrive
+                // step i+kDepth's data: kDepth steps of MFMAs to arrive
                 mfmas_k(kd[0], std::integral_constant<int, 1>{}, [&] {
-                    load_x(i + 1 + nTR, cur);
-                    load_dy(i + 2, cur);
+                    load_x(i + kDepth + nTR - 1, cur);
+                    load_dy(i + kDepth, cur);
                 });
             } else if constexpr (kq == NK - 1) {
                 // step i+1's data (loaded during step i-1) into slots this step does not read
@@ -366,27 +402,47 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
         });
         __syncthreads();
     };
+    // unrolled by kDepth so that every buffer index is a constant: step i+j
+    // loads into buffer j (step i+j+kDepth) and stores buffer j+1 (step i+j+1)
     int i = 0;
-    for (; i + 1 < nrows; i += 2) {
-        step(i, bufA, bufB);
-        step(i + 1, bufB, bufA);
-    }
-    if (i < nrows) step(i, bufA, bufB);
+    for (; i + kDepth <= nrows; i += kDepth)
+        static_for<0, kDepth>([&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            step(i + j, buf[j], buf[(j + 1) % kDepth]);
+        });
+    static_for<0, kDepth - 1>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        if (i + j < nrows) step(i + j, buf[j], buf[(j + 1) % kDepth]);
+    });
 #pragma unroll
-    for (int i = 0; i < TRB; ++i)
-#pragma unroll
-        for (int j = 0; j < SS; ++j) mfma_drain(acc[i][j]);
+    for (int j = 0; j < FCNT; ++j) mfma_drain(acc[j]);
 
-    // partial in fragment order: [chunk][gy][gz][wave][tr][s][16][64]
+    // partial in fragment order: kBlock64 [chunk][gy][gz][wave][tap][16][64],
+    // kTapSplit [chunk][gy][gz][tap][16][64] (tap = tr * SS + s)
+    const int64_t blk = int64_t(blockIdx.y) * a.gz + blockIdx.z;
     float* part = a.part + int64_t(blockIdx.x) * a.F +
-                  ((int64_t(blockIdx.y) * a.gz + blockIdx.z) * 4 + wave) * TRB * SS * 1024;
+                  (MODE == kBlock64 ? (blk * 4 + wave) * NT : blk * NT + FST) * 1024;
 #pragma unroll
-    for (int tr = 0; tr < TRB; ++tr) {
+    for (int j = 0; j < FCNT; ++j)
 #pragma unroll
-        for (int s = 0; s < SS; ++s)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                part[(tr * SS + s) * 1024 + e * 64 + lane] = acc[tr][s][e];
+        for (int e = 0; e < 16; ++e) part[j * 1024 + e * 64 + lane] = acc[j][e];
+}
+
+template <int SS, int TRB>
+__global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    strip_body<SS, TRB, kBlock64, 0>(a, smem);
+}
+
+// the wave index selects the (compile-time) tap run; the branch is uniform
+template <int SS, int TRB>
+__global__ __launch_bounds__(kThreads) void wgrad_taps_bf16_kernel(WgradArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    switch (threadIdx.x >> 6) {
+        case 0: strip_body<SS, TRB, kTapSplit, 0>(a, smem); break;
+        case 1: strip_body<SS, TRB, kTapSplit, 1>(a, smem); break;
+        case 2: strip_body<SS, TRB, kTapSplit, 2>(a, smem); break;
+        default: strip_body<SS, TRB, kTapSplit, 3>(a, smem); break;
     }
 }
 
@@ -671,7 +727,22 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
     const int l = threadIdx.x;
     const float total = ((red[0][l] + red[1][l]) + red[2][l]) + red[3][l];
     int64_t idx;
-    if (a.frag) {
+    if (a.frag == 2) {
+        // [gy][gz][tap][16][64] -> (o, ci, r, s), 32x32 blocks
+        const int NT = a.TRB * a.S;
+        int64_t t = f;
+        const int lane = int(t % 64); t /= 64;
+        const int e = int(t % 16); t /= 16;
+        const int tap = int(t % NT); t /= NT;
+        const int bz = int(t % a.gz);
+        const int by = int(t / a.gz);
+        const int ncsb = (a.C + 31) / 32;
+        const int o = (bz / ncsb) * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
+        const int ci = (bz % ncsb) * 32 + (lane & 31);
+        const int r = by * a.TRB + tap / a.S, s = tap % a.S;
+        if (r >= a.R || o >= a.K || ci >= a.C) return;
+        idx = ((int64_t(o) * a.C + ci) * a.R + r) * a.S + s;
+    } else if (a.frag) {
         // [gy][gz][wave][tr][s][16][64] -> (o, ci, r, s)
         const int SS = a.S;
         int64_t t = f;
@@ -710,6 +781,14 @@ static hipError_t launch_strip(const WgradArgs& a, dim3 grid, hipStream_t s) {
 }
 
 template <int SS>
+static hipError_t launch_taps(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    hipError_t e = set_lds(wgrad_taps_bf16_kernel<SS, SS>, a.lds_bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((wgrad_taps_bf16_kernel<SS, SS>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
+template <int SS>
 static hipError_t launch_rows_bf16(const WgradArgs& a, dim3 grid, hipStream_t s) {
     constexpr int TRB = SS == 1 ? 9 : (9 / SS > 0 ? 9 / SS : 1);
     hipError_t e = set_lds(wgrad_rows_bf16_kernel<SS, TRB>, a.lds_bytes);
@@ -731,6 +810,16 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
         DC_STRIP(5, 1) DC_STRIP(6, 1) DC_STRIP(7, 1)
         return hipErrorInvalidValue;
 #undef DC_STRIP
+    } else if (a.kind == WGRAD_TAPS_BF16) {
+        switch (a.S) {
+            case 2: e = launch_taps<2>(a, grid, s); break;
+            case 3: e = launch_taps<3>(a, grid, s); break;
+            case 4: e = launch_taps<4>(a, grid, s); break;
+            case 5: e = launch_taps<5>(a, grid, s); break;
+            case 6: e = launch_taps<6>(a, grid, s); break;
+            case 7: e = launch_taps<7>(a, grid, s); break;
+            default: return hipErrorInvalidValue;
+        }
     } else if (a.kind == WGRAD_ROWS_BF16) {
         switch (a.S) {
             case 1: e = launch_rows_bf16<1>(a, grid, s); break;

@@ -85,6 +85,11 @@ SMALL = {
     "s2dec_bf16": Layer("s2dec_bf16", 2, 16, 32, 32, 32, 3, 3, 2, 1, 2, 2, 1, "bf16", "uniform", 88),
     "s2k7dec_f32": Layer("s2k7dec_f32", 1, 3, 8, 32, 32, 7, 7, 2, 3, 2, 2, 3, "f32", "uniform", 89),
     "s2k1dec_bf16": Layer("s2k1dec_bf16", 2, 32, 48, 32, 32, 1, 1, 2, 0, 2, 2, 0, "bf16", "uniform", 90),
+    # at most 32 channels and filters: the weight gradient deals the taps of
+    # one 32x32 block to the four waves (partial blocks, partial strips)
+    "taps3_bf16": Layer("taps3_bf16", 2, 16, 24, 40, 40, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 91),
+    "taps5_bf16": Layer("taps5_bf16", 2, 32, 20, 36, 52, 5, 5, 1, 2, 2, 2, 2, "bf16", "uniform", 92),
+    "taps7_bf16": Layer("taps7_bf16", 1, 8, 32, 48, 48, 7, 7, 1, 3, 2, 2, 3, "bf16", "uniform", 93),
 }
 
 
@@ -133,7 +138,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
-                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32"])
+                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
@@ -146,7 +151,7 @@ def test_integer_inputs_are_bit_exact(name):
     _check("dw", dwg, dwr, L.dtype, exact=True)
 
 
-@pytest.mark.parametrize("name", ["c2", "odd_bf16", "c5b_s", "s2k7dec_f32"])
+@pytest.mark.parametrize("name", ["c2", "odd_bf16", "c5b_s", "s2k7dec_f32", "taps7_bf16"])
 def test_single_tile_calls_match_all_tiles(name):
     """Per-tile pack -> emulated exchange (region copies) -> unpack -> passes
     equals the all-tiles launch bit for bit, and accumulate=1 sums the tiles."""
