@@ -88,6 +88,28 @@ __device__ __forceinline__ uint4 window8_rt(const uint32_t (&d)[8], int sh) {
     }
 }
 
+// The same window for a shift known only at run time (0..7, equal on every
+// lane), without branches: selects pick the whole dwords, a byte-align the
+// odd element.  Straight-line code lets the scheduler interleave it with
+// matrix instructions.
+__device__ __forceinline__ uint4 window8_sel(const uint32_t (&d)[8], int sh) {
+    const int k = sh >> 1;
+    const uint32_t bs = uint32_t(sh & 1) * 2u;
+    uint32_t w[5];
+#pragma unroll
+    for (int j = 0; j < 5; ++j) {
+        const uint32_t a = k & 1 ? d[j + 1] : d[j];
+        const uint32_t b = k & 1 ? d[j + 3] : d[j + 2];
+        w[j] = k & 2 ? b : a;
+    }
+    uint4 r;
+    r.x = __builtin_amdgcn_alignbyte(w[1], w[0], bs);
+    r.y = __builtin_amdgcn_alignbyte(w[2], w[1], bs);
+    r.z = __builtin_amdgcn_alignbyte(w[3], w[2], bs);
+    r.w = __builtin_amdgcn_alignbyte(w[4], w[3], bs);
+    return r;
+}
+
 // 8 consecutive bf16 of a row starting at column g0 + sh, where g0 is a
 // multiple of 8 and sh (0..7) is the same for the whole wave; columns outside
 // [0, ncols) read as zero.  `row` is 16-byte aligned with `pitch` (a multiple

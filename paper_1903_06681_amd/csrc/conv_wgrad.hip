@@ -162,23 +162,38 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
 
 // ---------------------------------------------------------------- strip kernel (bf16)
 
-// Two ways to share a workgroup's block among its four waves:
-//  * kBlock64: 64 filters x 64 channels; wave = (filter half, channel half),
-//    each wave accumulates its 32 x 32 block at every tap of the row group;
-//  * kTapSplit: one 32 x 32 block (small channel counts); the row group's
-//    taps (row-major) are dealt to the waves in four contiguous runs, so a
-//    wave reads only the x rows its taps touch.
-enum StripMode { kBlock64 = 0, kTapSplit = 1 };
+// Three ways to share a workgroup's block among its waves:
+//  * kBlock64 (4 waves): 64 filters x 64 channels; wave = (filter half,
+//    channel half), each wave accumulates its 32 x 32 block at every tap of
+//    the row group;
+//  * kPair64 (8 waves): the same block, two waves per 32 x 32 sub-block that
+//    split its taps (first half / second half, row-major).  Two waves per
+//    SIMD: one wave's LDS reads, byte-aligns and staging issue while the
+//    other's matrix instructions run, which a single wave cannot overlap;
+//  * kTapSplit (4 waves): one 32 x 32 block (small channel counts); the row
+//    group's taps are dealt to the waves in four contiguous runs.
+// In every mode a wave reads only the x rows its taps touch.
+enum StripMode { kBlock64 = 0, kTapSplit = 1, kPair64 = 2 };
 
 template <int MODE, int NT>
-struct TapRange {   // taps [first(W), first(W) + count(W)) of wave W
-    static constexpr int first(int W) { return MODE == kBlock64 ? 0 : W * (NT / 4) + (W < NT % 4 ? W : NT % 4); }
-    static constexpr int count(int W) { return MODE == kBlock64 ? NT : NT / 4 + (W < NT % 4 ? 1 : 0); }
+struct TapRange {   // taps [first(W), first(W) + count(W)) of wave group W
+    static constexpr int first(int W) {
+        return MODE == kBlock64 ? 0
+             : MODE == kPair64  ? (W == 0 ? 0 : (NT + 1) / 2)
+                                : W * (NT / 4) + (W < NT % 4 ? W : NT % 4);
+    }
+    static constexpr int count(int W) {
+        return MODE == kBlock64 ? NT
+             : MODE == kPair64  ? (W == 0 ? (NT + 1) / 2 : NT / 2)
+                                : NT / 4 + (W < NT % 4 ? 1 : 0);
+    }
 };
+template <int MODE> struct StripThreads { static constexpr int value = MODE == kPair64 ? 512 : 256; };
 
 template <int SS, int TRB, int MODE, int W>
 __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* smem) {
-    constexpr int CB = MODE == kBlock64 ? 64 : 32;          // channels / filters staged
+    constexpr int CB = MODE == kTapSplit ? 32 : 64;         // channels / filters staged
+    constexpr int NTH = StripThreads<MODE>::value;
     constexpr int NR = TRB + 1;                             // x ring slots
     uint16_t* xring = reinterpret_cast<uint16_t*>(smem);    // [NR][CB ci][kXP]
     uint16_t* dyb = xring + NR * CB * kXP;                  // [2][CB o][kXP]
@@ -201,7 +216,7 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int l32 = lane & 31, hi = lane >> 5;
-    const int ow = MODE == kBlock64 ? wave & 1 : 0, cw = MODE == kBlock64 ? wave >> 1 : 0;
+    const int ow = MODE == kTapSplit ? 0 : wave & 1, cw = MODE == kTapSplit ? 0 : (wave >> 1) & 1;
 
     const uint16_t* xt = static_cast<const uint16_t*>(a.x) + tile * a.x_tile +
                          int64_t(n) * a.C * a.x_rows * a.x_pitch;
@@ -218,7 +233,8 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
 
     // staging units: x row = CB channels x 9 groups of 8; dy row = CB filters x 8 groups
     constexpr int XU = CB * 9, DU = CB * 8;
-    constexpr int XPT = (XU + kThreads - 1) / kThreads, DPT = DU / kThreads;
+    constexpr int XPT = (XU + NTH - 1) / NTH, DPT = DU / NTH;
+    static_assert(DPT * NTH == DU, "dy units must spread evenly over the threads");
     // Staging in two phases so that global loads overlap the MFMAs:
     // load_*() only issues unconditional 16-byte loads from clamped addresses
     // into registers; store_*() (after the next row's MFMAs) shifts the
@@ -236,7 +252,7 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
         const int gr = min(max(xrow0 + m, 0), a.x_rows - 1);
 #pragma unroll
         for (int k = 0; k < XPT; ++k) {
-            const int u = min(tid + k * kThreads, XU - 1);
+            const int u = min(tid + k * NTH, XU - 1);
             const int ci = u / 9, g8 = u - ci * 9;
             const int gc = min(xg0 + 8 * g8, a.x_pitch - 8);
             r.x[k] = *reinterpret_cast<const uint4*>(xt + min(c0 + ci, a.C - 1) * xplane +
@@ -247,21 +263,21 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
         uint16_t* slot = xring + (m % NR) * CB * kXP;
         const int gr = xrow0 + m;
         const bool rok = gr >= 0 && gr < a.x_rows;
+        // units past XU repeat unit XU-1 (same clamped load, same mask): the
+        // duplicate stores write identical bytes, and need no branch
 #pragma unroll
         for (int k = 0; k < XPT; ++k) {
-            const int u = tid + k * kThreads;
-            if (u < XU) {
-                const int ci = u / 9, g8 = u - ci * 9;
-                const int nv = (rok && c0 + ci < a.C) ? a.x_cols - (xg0 + 8 * g8) : 0;
-                *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = mask8(r.x[k], nv);
-            }
+            const int u = min(tid + k * NTH, XU - 1);
+            const int ci = u / 9, g8 = u - ci * 9;
+            const int nv = (rok && c0 + ci < a.C) ? a.x_cols - (xg0 + 8 * g8) : 0;
+            *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = mask8(r.x[k], nv);
         }
     };
     auto load_dy = [&](int i, Regs& r) {   // output row p0 + i -> registers (clamped)
         const int gr = min(p0 + i + a.dy_off, dy_rows - 1);
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
-            const int u = tid + k * kThreads;
+            const int u = tid + k * NTH;
             const int o = u >> 3, g8 = u & 7;
             const uint16_t* row = dyt + min(o0 + o, a.K - 1) * dyplane + int64_t(gr) * a.dy_pitch;
             const int ga = dya0 + 8 * g8;
@@ -273,13 +289,11 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
         uint16_t* slot = dyb + (i & 1) * CB * kXP;
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
-            const int u = tid + k * kThreads;
+            const int u = tid + k * NTH;
             const int o = u >> 3, g8 = u & 7;
-            uint4 v = r.d0[k];
-            if (dysh != 0) {
-                const uint32_t d[8] = {v.x, v.y, v.z, v.w, r.d1[k].x, r.d1[k].y, r.d1[k].z, r.d1[k].w};
-                v = window8_rt(d, dysh);
-            }
+            const uint4 v0 = r.d0[k];
+            const uint32_t d[8] = {v0.x, v0.y, v0.z, v0.w, r.d1[k].x, r.d1[k].y, r.d1[k].z, r.d1[k].w};
+            const uint4 v = window8_sel(d, dysh);
             const int nv = (o0 + o < a.K) ? dy_end - (dyg0 + 8 * g8) : 0;
             *reinterpret_cast<uint4*>(slot + o * kXP + 8 * g8) = mask8(v, nv);
         }
@@ -417,11 +431,11 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
 #pragma unroll
     for (int j = 0; j < FCNT; ++j) mfma_drain(acc[j]);
 
-    // partial in fragment order: kBlock64 [chunk][gy][gz][wave][tap][16][64],
+    // partial in fragment order: kBlock64 / kPair64 [chunk][gy][gz][sub-block][tap][16][64],
     // kTapSplit [chunk][gy][gz][tap][16][64] (tap = tr * SS + s)
     const int64_t blk = int64_t(blockIdx.y) * a.gz + blockIdx.z;
     float* part = a.part + int64_t(blockIdx.x) * a.F +
-                  (MODE == kBlock64 ? (blk * 4 + wave) * NT : blk * NT + FST) * 1024;
+                  (MODE == kTapSplit ? blk * NT + FST : (blk * 4 + (wave & 3)) * NT + FST) * 1024;
 #pragma unroll
     for (int j = 0; j < FCNT; ++j)
 #pragma unroll
@@ -435,6 +449,15 @@ __global__ __launch_bounds__(kThreads) void wgrad_strip_bf16_kernel(WgradArgs a)
 }
 
 // the wave index selects the (compile-time) tap run; the branch is uniform
+template <int SS, int TRB>
+__global__ __launch_bounds__(512) void wgrad_pair_bf16_kernel(WgradArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    if (threadIdx.x < 256)
+        strip_body<SS, TRB, kPair64, 0>(a, smem);
+    else
+        strip_body<SS, TRB, kPair64, 1>(a, smem);
+}
+
 template <int SS, int TRB>
 __global__ __launch_bounds__(kThreads) void wgrad_taps_bf16_kernel(WgradArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -772,11 +795,19 @@ static hipError_t set_lds(K kernel, int bytes) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
+// one filter tap per workgroup: four waves, each with its whole 32x32 block;
+// more taps: eight waves, two per sub-block
 template <int SS, int TRB>
 static hipError_t launch_strip(const WgradArgs& a, dim3 grid, hipStream_t s) {
-    hipError_t e = set_lds(wgrad_strip_bf16_kernel<SS, TRB>, a.lds_bytes);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((wgrad_strip_bf16_kernel<SS, TRB>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    if constexpr (SS * TRB == 1) {
+        hipError_t e = set_lds(wgrad_strip_bf16_kernel<SS, TRB>, a.lds_bytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((wgrad_strip_bf16_kernel<SS, TRB>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    } else {
+        hipError_t e = set_lds(wgrad_pair_bf16_kernel<SS, TRB>, a.lds_bytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((wgrad_pair_bf16_kernel<SS, TRB>), grid, dim3(512), a.lds_bytes, s, a);
+    }
     return hipGetLastError();
 }
 
