@@ -139,16 +139,26 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
         if (a.wvec && a.wmode == 0) {
             // rows o0 .. o0+OBT-1 of w are consecutive: 16-byte chunks straight to
             // LDS, all of a thread's loads in flight at once (chunks of rows
-            // past Cout re-read the last valid chunk)
+            // past Cout re-read the last valid chunk).  Every workgroup reads
+            // the same block at the same moment; each starts at its own
+            // offset so that the requests spread over the L2 channels
+            // instead of queueing on the few that hold the first lines.
             constexpr int CPR = RL / 8, NCH = OBT * CPR, NB = (NCH + kWThreads - 1) / kWThreads;
             const int last = nO * CPR - 1;
+            const int rot = ((blockIdx.x % 16) * (NB / 16 > 0 ? NB / 16 : 1) % NB) * kWThreads;   // < NB * kWThreads
             const uint4* src = reinterpret_cast<const uint4*>(w + int64_t(o0) * RL);
             uint4 buf[NB];
-#pragma unroll
-            for (int b = 0; b < NB; ++b) buf[b] = src[min(b * kWThreads + tid, last)];
+            int vv[NB];
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
-                const int v = b * kWThreads + tid;
+                int v = b * kWThreads + tid + rot;
+                v = v >= NB * kWThreads ? v - NB * kWThreads : v;
+                vv[b] = v;
+                buf[b] = src[min(v, last)];
+            }
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int v = vv[b];
                 if (v < NCH) *reinterpret_cast<uint4*>(Wl + (v / CPR) * PW + (v % CPR) * 8) = buf[b];
             }
         } else if (a.wvec) {
@@ -163,10 +173,16 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
             if (tid < TPR * CPR) {
                 const int c = tid % CPR, r0 = tid / CPR;
                 const uint16_t* src = w + min(int64_t(o0) * T + c * 8, last);
+                // buffer slot r holds row group (r + rot) mod NR: the workgroups
+                // start their reads at different rows (see the forward copy)
+                const int rot = blockIdx.x % NR;
                 uint4 buf[NR];
+                int rrow[NR];
 #pragma unroll
-                for (int r = 0; r < NR; ++r)
-                    buf[r] = *reinterpret_cast<const uint4*>(src + min(r0 + r * TPR, CIN - 1) * rs);
+                for (int r = 0; r < NR; ++r) {
+                    rrow[r] = r + rot < NR ? r + rot : r + rot - NR;
+                    buf[r] = *reinterpret_cast<const uint4*>(src + min(r0 + rrow[r] * TPR, CIN - 1) * rs);
+                }
                 uint16_t* dst[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
@@ -175,11 +191,12 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 }
 #pragma unroll
                 for (int r = 0; r < NR; ++r) {
-                    if (r0 + r * TPR < CIN) {
+                    if (r0 + rrow[r] * TPR < CIN) {
                         Pack8 pk;
                         pk.v = buf[r];
+                        const int off = rrow[r] * TPR * T;
 #pragma unroll
-                        for (int j = 0; j < 8; ++j) dst[j][r * TPR * T] = pk.h[j];
+                        for (int j = 0; j < 8; ++j) dst[j][off] = pk.h[j];
                     }
                 }
             }

@@ -263,14 +263,17 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
         uint16_t* slot = xring + (m % NR) * CB * kXP;
         const int gr = xrow0 + m;
         const bool rok = gr >= 0 && gr < a.x_rows;
-        // units past XU repeat unit XU-1 (same clamped load, same mask): the
-        // duplicate stores write identical bytes, and need no branch
+        // With several taps the staging stays branch-free, so that it can sit
+        // in the MFMA stream: units past XU repeat unit XU-1 (same clamped
+        // load, same mask) and their duplicate stores write identical bytes.
+        // A single tap leaves nothing to overlap: skip the duplicates.
 #pragma unroll
         for (int k = 0; k < XPT; ++k) {
             const int u = min(tid + k * NTH, XU - 1);
             const int ci = u / 9, g8 = u - ci * 9;
             const int nv = (rok && c0 + ci < a.C) ? a.x_cols - (xg0 + 8 * g8) : 0;
-            *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = mask8(r.x[k], nv);
+            if (NT > 1 || tid + k * NTH < XU)
+                *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) = mask8(r.x[k], nv);
         }
     };
     auto load_dy = [&](int i, Regs& r) {   // output row p0 + i -> registers (clamped)
@@ -293,7 +296,11 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
             const int o = u >> 3, g8 = u & 7;
             const uint4 v0 = r.d0[k];
             const uint32_t d[8] = {v0.x, v0.y, v0.z, v0.w, r.d1[k].x, r.d1[k].y, r.d1[k].z, r.d1[k].w};
-            const uint4 v = window8_sel(d, dysh);
+            uint4 v = v0;
+            if constexpr (NT > 1)
+                v = window8_sel(d, dysh);
+            else if (dysh != 0)
+                v = window8_rt(d, dysh);
             const int nv = (o0 + o < a.K) ? dy_end - (dyg0 + 8 * g8) : 0;
             *reinterpret_cast<uint4*>(slot + o * kXP + 8 * g8) = mask8(v, nv);
         }
