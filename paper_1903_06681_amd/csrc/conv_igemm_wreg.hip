@@ -120,18 +120,23 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     if (NPRE > 1) load_rows(stg1, 2, min(2, TR - 1));
 
     // ---- weights -> A-fragments, in two passes:
-    //  1. the workgroup's block of w goes to LDS as Wl[o][ci][t'] (rows of
-    //     CIN*T elements, pitch PW), t' the tap in k-step order:
-    //       forward:       Wl[o][ci][t]       = w[o0+o][ci][t]
-    //       backward-data: Wl[o][ci][T-1-t]   = w[ci][o0+o][t]   (flipped taps)
+    //  1. the workgroup's block of w goes to LDS, rows o of pitch PW:
+    //       forward:       Wl[o][ci][t] = w[o0+o][ci][t]   (w's own order: a
+    //                      straight 16-byte copy)
+    //       backward-data: Wl[o][t][ci] = w[ci][o0+o][t]   (tap-major: the
+    //                      transpose of w's first two axes is written by
+    //                      lanes = consecutive ci, i.e. contiguous LDS bytes)
     //     rows o >= Cout - o0 hold whatever was read: they only feed output
     //     channels that are never stored;
-    //  2. each lane reads, per (output block, 16-channel group), the 8
-    //     channels x T taps of its row and channel half (16*T contiguous
-    //     bytes) and regroups them in registers into T fragments.
+    //  2. each lane builds, per (output block, 16-channel group), its T
+    //     fragments of 8 channels: forward from its 8 channels x T taps
+    //     (16*T contiguous bytes) regrouped with byte permutes; backward-data
+    //     one aligned 16-byte read per fragment, the taps taken in reverse
+    //     order (the flip of Eq. (3)).
     constexpr int T = TR * TS;
     constexpr int RL = CIN * T;                                    // row length
     constexpr int PW = ((RL * 2 + 239) / 256 * 256 + 16) / 2;      // 2*PW = 16 (mod 256)
+    constexpr int PWB = ((RL * 2 + 111) / 128 * 128 + 16) / 2;     // 2*PWB = 16 (mod 128)
     const int nO = min(OBT, a.Cout - o0);                         // valid output channels here
     uint16_t* Wl = lds;
     {
@@ -163,40 +168,38 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
             }
         } else if (a.wvec) {
             // row ci of w holds (o, t) of this block as OBT*T consecutive
-            // elements.  Each thread keeps one 16-byte chunk position c of the
-            // rows and walks rows ci = r0, r0 + TPR, ...: the LDS positions of
-            // its chunk's 8 elements are then per-thread constants plus a
-            // compile-time row offset.
-            constexpr int CPR = OBT * T / 8, TPR = kWThreads / CPR, NR = (CIN + TPR - 1) / TPR;
+            // elements (16-byte chunks c).  A thread takes 8x8 blocks (8 rows
+            // ci x one chunk), loads the 8 chunks (consecutive threads:
+            // consecutive chunks of the same rows), transposes them in
+            // registers and writes 8 aligned 16-byte vectors Wl[o][t][ci..ci+7].
+            // The workgroups start at different blocks (see the forward copy).
+            constexpr int CPR = OBT * T / 8, NBLK = (CIN / 8) * CPR;
+            constexpr int NB = (NBLK + kWThreads - 1) / kWThreads;
             const int64_t rs = int64_t(a.Cout) * T;                 // w row stride
             const int64_t last = int64_t(a.Cout) * T - 8;           // last chunk start in a row
-            if (tid < TPR * CPR) {
-                const int c = tid % CPR, r0 = tid / CPR;
-                const uint16_t* src = w + min(int64_t(o0) * T + c * 8, last);
-                // buffer slot r holds row group (r + rot) mod NR: the workgroups
-                // start their reads at different rows (see the forward copy)
-                const int rot = blockIdx.x % NR;
-                uint4 buf[NR];
-                int rrow[NR];
+            const int rot = (blockIdx.x % NB) * kWThreads;
+            uint4 blk[NB][8];
+            int bid[NB];
 #pragma unroll
-                for (int r = 0; r < NR; ++r) {
-                    rrow[r] = r + rot < NR ? r + rot : r + rot - NR;
-                    buf[r] = *reinterpret_cast<const uint4*>(src + min(r0 + rrow[r] * TPR, CIN - 1) * rs);
-                }
-                uint16_t* dst[8];
+            for (int b = 0; b < NB; ++b) {
+                int v = b * kWThreads + tid + rot;
+                v = v >= NB * kWThreads ? v - NB * kWThreads : v;
+                bid[b] = v;
+                const int vc = min(v, NBLK - 1), g = vc / CPR, c = vc - g * CPR;
+                const uint16_t* src = w + min(int64_t(o0) * T + c * 8, last) + int64_t(g * 8) * rs;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int e = c * 8 + j, o = e / T, t = e % T;
-                    dst[j] = Wl + o * PW + r0 * T + (T - 1 - t);
-                }
+                for (int r = 0; r < 8; ++r) blk[b][r] = *reinterpret_cast<const uint4*>(src + r * rs);
+            }
 #pragma unroll
-                for (int r = 0; r < NR; ++r) {
-                    if (r0 + rrow[r] * TPR < CIN) {
-                        Pack8 pk;
-                        pk.v = buf[r];
-                        const int off = rrow[r] * TPR * T;
+            for (int b = 0; b < NB; ++b) {
+                if (bid[b] < NBLK) {
+                    const int g = bid[b] / CPR, c = bid[b] - g * CPR;
+                    uint4 t8[8];
+                    transpose8x8(blk[b], t8);
 #pragma unroll
-                        for (int j = 0; j < 8; ++j) dst[j][off] = pk.h[j];
+                    for (int q = 0; q < 8; ++q) {
+                        const int e = c * 8 + q, o = e / T, t = e - o * T;
+                        *reinterpret_cast<uint4*>(Wl + o * PWB + t * CIN + g * 8) = t8[q];
                     }
                 }
             }
@@ -205,14 +208,22 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
             for (int e = tid; e < OBT * RL; e += kWThreads) {
                 const int o = e / RL, r = e % RL, ci = r / T, t = r % T;
                 const int oc = min(o0 + o, a.Cout - 1);
-                Wl[o * PW + r] = a.wmode ? w[(int64_t(ci) * a.Cout + oc) * T + (T - 1 - t)]
-                                         : w[(int64_t(oc) * CIN + ci) * T + t];
+                if (a.wmode)
+                    Wl[o * PWB + t * CIN + ci] = w[(int64_t(ci) * a.Cout + oc) * T + t];
+                else
+                    Wl[o * PW + r] = w[(int64_t(oc) * CIN + ci) * T + t];
             }
         }
     }
     __syncthreads();
     bf16x8 Wf[NOB][KS];
-    static_for<0, NOB * CG>([&](auto gc) {
+    if (a.wmode) {
+        static_for<0, NOB * KS>([&](auto fc) {
+            constexpr int f = decltype(fc)::value, ob = f % NOB, k = f / NOB, t = k / CG, cg = k % CG;
+            Wf[ob][k] = *reinterpret_cast<const bf16x8*>(Wl + (ob * 32 + l32) * PWB + (T - 1 - t) * CIN +
+                                                         cg * 16 + 8 * hi);
+        });
+    } else static_for<0, NOB * CG>([&](auto gc) {
         constexpr int g = decltype(gc)::value, ob = g / CG, cg = g % CG;
         const uint16_t* row = Wl + (ob * 32 + l32) * PW + (cg * 16 + 8 * hi) * T;
         uint32_t seg[4 * T];   // element c*T + t: channel c of the 8, tap t
@@ -370,8 +381,9 @@ static int wreg_lds(int NOB, int TR, int TS, int CG) {
     const int CIN = CG * 16, PS = 8 * ((CIN / 8) | 1), RPX8 = (64 + TS - 1 + 7) / 8;
     const int ring = (TR + 3) * RPX8 * 8 * PS * 2;
     const int RL = CIN * TR * TS;
-    const int PW = ((RL * 2 + 239) / 256 * 256 + 16) / 2;
-    const int wl = NOB * 32 * PW * 2;
+    const int PW = ((RL * 2 + 239) / 256 * 256 + 16) / 2;       // forward weight rows
+    const int PWB = ((RL * 2 + 111) / 128 * 128 + 16) / 2;      // backward-data weight rows
+    const int wl = NOB * 32 * (PW > PWB ? PW : PWB) * 2;
     return ring > wl ? ring : wl;
 }
 
