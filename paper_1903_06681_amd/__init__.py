@@ -20,6 +20,12 @@ if not os.path.exists(LIB_PATH):
         f"{LIB_PATH} is missing: build the HIP library first "
         "(python -c 'import __graft_entry__ as g; g.build()')")
 
+# torch brings its own HIP runtime (same soname as /opt/rocm's).  Loading it
+# first makes libdc.so bind to that one copy: with the library loaded first,
+# the process would hold two runtimes, and pointers and streams from torch
+# would be foreign to the library's launches.
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 DC_F32, DC_BF16 = 0, 1

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <vector>
 
 #include "dc.h"
 #include "geometry.h"
@@ -123,6 +124,11 @@ static dc_status launched(hipError_t e) {
     return hipGetLastError() == hipSuccess ? DC_OK : DC_ERR_HIP;
 }
 
+// hipGetLastError reports the last error of any earlier HIP call on this
+// thread, including the caller's own; clear it before launching so that only
+// this call's launches can turn into DC_ERR_HIP.
+static void clear_stale_error() { (void)hipGetLastError(); }
+
 // ---------------------------------------------------------------- halo
 
 static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which,
@@ -151,6 +157,7 @@ static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which
     a.tile0 = a.all_tiles ? 0 : tile;
     a.ntiles = a.all_tiles ? g.ntiles : 1;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    clear_stale_error();
     return launched(unpack ? launch_halo_unpack(a, g.esize, s) : launch_halo_pack(a, g.esize, s));
 }
 
@@ -283,6 +290,7 @@ dc_status dc_conv_fwd(const dc_problem* prob, int32_t tile, const void* x_pad,
     a.w_os = int64_t(g.C) * g.R * g.S; a.w_cs = int64_t(g.R) * g.S;
     a.wmode = 0;
     if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+    clear_stale_error();
     return launched(launch_igemm(a, g.dtype, static_cast<hipStream_t>(stream)));
 }
 
@@ -299,6 +307,7 @@ dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_
     // is a stride-1 correlation of dy with the taps r = (phase+pad) mod stride
     // + stride*t, visited in reverse.  At stride 1 there is one phase holding
     // the whole filter reversed.
+    std::vector<IgemmArgs> phases;
     for (int phr = 0; phr < st_; ++phr) {
         for (int phc = 0; phc < st_; ++phc) {
             IgemmArgs a;
@@ -325,9 +334,15 @@ dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_
             a.w_os = int64_t(g.R) * g.S; a.w_cs = int64_t(g.C) * g.R * g.S;
             a.wmode = 1;
             if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
-            dc_status r = launched(launch_igemm(a, g.dtype, s));
-            if (r != DC_OK) return r;
+            phases.push_back(a);
         }
+    }
+    // every phase is planned before the first launch: an unsupported one
+    // launches nothing
+    clear_stale_error();
+    for (const IgemmArgs& a : phases) {
+        dc_status r = launched(launch_igemm(a, g.dtype, s));
+        if (r != DC_OK) return r;
     }
     return DC_OK;
 }
@@ -367,6 +382,7 @@ dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x
     a.base_r = g.h - g.pad; a.base_c = g.h - g.pad;
     a.accumulate = accumulate;
     if (!wgrad_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+    clear_stale_error();
     return launched(launch_wgrad(a, g.dtype, static_cast<hipStream_t>(stream)));
 }
 

@@ -260,6 +260,46 @@ def test_unpack_writes_only_margins():
 
 # ------------------------------------------------------------------ properties
 
+def test_stale_hip_error_of_the_caller_is_not_reported():
+    """hipGetLastError keeps the last error of any earlier HIP call: an error
+    the caller left behind must not make the next library call fail.  Each
+    call below runs right after an invalid hipSetDevice has set that error."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+
+    def stale():
+        assert hip.hipSetDevice(ctypes.c_int(1 << 20)) != 0   # invalid ordinal
+
+    L = SMALL["odd_bf16"]
+    p = dc.Problem.of(L)
+    nt = L.P * L.Q
+    x, w, dy = (wl.draw(L, t) for t in ("x", "w", "dy"))
+    xt = H.alloc_tiles(p, X, nt, L.dtype)
+    dyt = H.alloc_tiles(p, DY, nt, L.dtype)
+    H.scatter_interiors(xt, H.to_device(x, L.dtype), p, X)
+    H.scatter_interiors(dyt, H.to_device(dy, L.dtype), p, DY)
+    wd = H.to_device(w, L.dtype)
+    y = torch.empty((nt, L.N, L.K, L.Hot, L.Wot), device="cuda")
+    dx = torch.empty((nt, L.N, L.C, L.Ht, L.Wt), device="cuda")
+    dw = torch.empty((L.K, L.C, L.R, L.S), device="cuda")
+    ws = torch.empty(max(dc.bwd_filter_workspace_bytes(p, ALL), 16), dtype=torch.uint8, device="cuda")
+    sx = torch.empty(nt * dc.halo_elems(p, X), dtype=H.TORCH_DT[L.dtype], device="cuda")
+    sdy = torch.empty(nt * dc.halo_elems(p, DY), dtype=H.TORCH_DT[L.dtype], device="cuda")
+    torch.cuda.synchronize()
+    for f in (lambda: dc.halo_pack(p, ALL, X, xt, sx), lambda: dc.halo_unpack(p, ALL, X, sx, xt),
+              lambda: dc.halo_pack(p, ALL, DY, dyt, sdy), lambda: dc.halo_unpack(p, ALL, DY, sdy, dyt),
+              lambda: dc.conv_fwd(p, ALL, xt, wd, y), lambda: dc.conv_bwd_data(p, ALL, dyt, wd, dx),
+              lambda: dc.conv_bwd_filter(p, ALL, xt, dyt, dw, 0, ws)):
+        stale()
+        f()
+    hip.hipGetLastError()
+    torch.cuda.synchronize()
+    yr, dxr, dwr = _oracle_full(L, x, w, dy)
+    _check("y", H.gather_outputs(y, p, "y").cpu().numpy(), yr, L.dtype)
+    _check("dx", H.gather_outputs(dx, p, "dx").cpu().numpy(), dxr, L.dtype)
+    _check("dw", dw.cpu().numpy(), dwr, L.dtype)
+
+
 def test_bwd_filter_ignores_dy_halo_and_is_deterministic():
     """dw needs no dy halo (Sec. III-A): NaN in every dy margin must not reach
     dw.  Two runs give identical bits (fixed-order reduction, no atomics)."""
