@@ -301,6 +301,22 @@ def main():
     total_ms = t0.elapsed_time(t1)
     ms_per_step = total_ms / args.steps
 
+    # the same step with every call on one stream: what the overlap of the dy
+    # exchange with the weight gradient saves
+    def serial_step():
+        for c in calls:
+            c()
+
+    for _ in range(2):
+        serial_step()
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        serial_step()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    serial_ms = t0.elapsed_time(t1) / args.steps
+
     # timed region 2: each pass K times back to back between two events on the
     # launch stream -> its average launch duration (an event pair around every
     # single call would add the event markers' own cost to each call)
@@ -394,6 +410,9 @@ def main():
         grid[n] = {"payload_bytes": payload, "ms": round(warm, 5),
                    "useful_GB/s": round(2 * payload / (warm * 1e-3) / 1e9, 1)}
     out["halo_all_tiles"] = grid
+    out["overlap"] = {"serial_step_ms": round(serial_ms, 5), "overlapped_step_ms": round(ms_per_step, 5),
+                      "saved_ms": round(serial_ms - ms_per_step, 5),
+                      "what": "dy halo pack/unpack on a second stream beside the weight gradient"}
 
     if not args.no_cold:
         # Cold timings: a 512 MB write (more than the 256 MB Infinity Cache and
