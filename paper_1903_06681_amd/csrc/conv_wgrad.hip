@@ -167,7 +167,8 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
 //    channel half), each wave accumulates its 32 x 32 block at every tap of
 //    the row group;
 //  * kPair64 (8 waves): the same block, two waves per 32 x 32 sub-block that
-//    split its taps (first half / second half, row-major).  Two waves per
+//    split its taps: by filter rows (first ceil(TRB/2) rows / the rest), so
+//    that the two read disjoint x rows, or, for one row, its taps.  Two waves per
 //    SIMD: one wave's LDS reads, byte-aligns and staging issue while the
 //    other's matrix instructions run, which a single wave cannot overlap;
 //  * kTapSplit (4 waves): one 32 x 32 block (small channel counts); the row
@@ -175,16 +176,18 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
 // In every mode a wave reads only the x rows its taps touch.
 enum StripMode { kBlock64 = 0, kTapSplit = 1, kPair64 = 2 };
 
-template <int MODE, int NT>
+template <int MODE, int TRB, int SS>
 struct TapRange {   // taps [first(W), first(W) + count(W)) of wave group W
+    static constexpr int NT = TRB * SS;
+    static constexpr int PAIR0 = TRB >= 2 ? (TRB + 1) / 2 * SS : (SS + 1) / 2;   // taps of group 0
     static constexpr int first(int W) {
         return MODE == kBlock64 ? 0
-             : MODE == kPair64  ? (W == 0 ? 0 : (NT + 1) / 2)
+             : MODE == kPair64  ? (W == 0 ? 0 : PAIR0)
                                 : W * (NT / 4) + (W < NT % 4 ? W : NT % 4);
     }
     static constexpr int count(int W) {
         return MODE == kBlock64 ? NT
-             : MODE == kPair64  ? (W == 0 ? (NT + 1) / 2 : NT / 2)
+             : MODE == kPair64  ? (W == 0 ? PAIR0 : NT - PAIR0)
                                 : NT / 4 + (W < NT % 4 ? 1 : 0);
     }
 };
@@ -198,7 +201,7 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
     uint16_t* xring = reinterpret_cast<uint16_t*>(smem);    // [NR][CB ci][kXP]
     uint16_t* dyb = xring + NR * CB * kXP;                  // [2][CB o][kXP]
     constexpr int NT = TRB * SS;                            // taps of the row group
-    constexpr int FST = TapRange<MODE, NT>::first(W), FCNT = TapRange<MODE, NT>::count(W);
+    constexpr int FST = TapRange<MODE, TRB, SS>::first(W), FCNT = TapRange<MODE, TRB, SS>::count(W);
     constexpr int RLO = FST / SS, NRW = (FST + FCNT - 1) / SS - RLO + 1;   // x rows this wave reads
 
     int c = blockIdx.x;
@@ -338,7 +341,7 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
     // per filter row the wave's taps touch, the 8 + (SS - 1) staged x
     // elements from which the SS shifted windows (B) are cut.  The LDS reads
     // of k-step kq+1 are issued before the MFMAs of k-step kq.
-    constexpr int XH = SS <= 5 ? 2 : 4;   // dwords read past the first 8 elements
+    constexpr int XH = SS <= 3 ? 1 : SS <= 5 ? 2 : 4;   // dwords read past the first 8 elements
     struct KData {
         uint4 A;
         uint32_t x[NRW][4 + XH];
@@ -360,7 +363,9 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
             for (int tr = 0; tr < NRW; ++tr) {
                 const uint4 lo = *reinterpret_cast<const uint4*>(xrows[tr] + qc);
                 d.x[tr][0] = lo.x; d.x[tr][1] = lo.y; d.x[tr][2] = lo.z; d.x[tr][3] = lo.w;
-                if constexpr (XH == 2) {
+                if constexpr (XH == 1) {
+                    d.x[tr][4] = *reinterpret_cast<const uint32_t*>(xrows[tr] + qc + 8);
+                } else if constexpr (XH == 2) {
                     const uint2 h = *reinterpret_cast<const uint2*>(xrows[tr] + qc + 8);
                     d.x[tr][4] = h.x; d.x[tr][5] = h.y;
                 } else {
