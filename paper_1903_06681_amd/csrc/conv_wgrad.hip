@@ -76,8 +76,17 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
                       int Hot, int Wot, int base_c, Plan* pl) {
     std::memset(pl, 0, sizeof(*pl));
     const bool xcol_aligned = base_c % 8 == 0;   // strip staging reads whole 16-byte x chunks
-    if (dtype == 1 && stride == 1 && S <= 7 && xcol_aligned) {
-        if (C <= 32 && K <= 32 && taps_filter(R, S)) {
+    const bool phase2 = dtype == 1 && stride == 2 && 4 * C <= 32 && xcol_aligned &&
+                        taps_filter((R + 1) / 2, (S + 1) / 2);
+    if ((dtype == 1 && stride == 1 && S <= 7 && xcol_aligned) || phase2) {
+        if (phase2) {
+            // the phase images: a stride-1 ceil(R/2) x ceil(S/2) filter on 4C channels
+            pl->kind = WGRAD_TAPS2_BF16;
+            pl->TRB = (R + 1) / 2;
+            pl->gy = 1;
+            pl->gz = (K + 31) / 32;
+            pl->frag = 3;
+        } else if (C <= 32 && K <= 32 && taps_filter(R, S)) {
             // one 32x32 block, every tap in one row group: x and dy are read once
             pl->kind = WGRAD_TAPS_BF16;
             pl->TRB = R;
@@ -103,7 +112,8 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
         pl->rows_per_seg = (Hot + nseg - 1) / nseg;
         pl->nseg = (Hot + pl->rows_per_seg - 1) / pl->rows_per_seg;
         pl->nchunks = strips * pl->nseg;
-        pl->F = int64_t(pl->gy) * pl->gz * (pl->frag == 1 ? 4 : 1) * pl->TRB * S * 1024;
+        const int SP = phase2 ? (S + 1) / 2 : S;   // filter width the kernel walks
+        pl->F = int64_t(pl->gy) * pl->gz * (pl->frag == 1 ? 4 : 1) * pl->TRB * SP * 1024;
         return true;
     }
     if (dtype == 1) {
@@ -145,7 +155,7 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
     a.chunks_per_tile = pl.chunks_per_tile; a.rows_per_chunk = pl.rows_per_chunk;
     a.nqb = pl.nqb; a.nseg = pl.nseg; a.rows_per_seg = pl.rows_per_seg;
     a.F = pl.F; a.frag = pl.frag;
-    if (a.kind == WGRAD_STRIP_BF16 || a.kind == WGRAD_TAPS_BF16) {
+    if (a.kind == WGRAD_STRIP_BF16 || a.kind == WGRAD_TAPS_BF16 || a.kind == WGRAD_TAPS2_BF16) {
         const int cb = a.kind == WGRAD_STRIP_BF16 ? 64 : 32;
         a.lds_bytes = ((a.TRB + 1) * cb * kXP + 2 * cb * kXP) * 2;
     } else if (a.kind == WGRAD_ROWS_BF16) {
@@ -193,7 +203,13 @@ struct TapRange {   // taps [first(W), first(W) + count(W)) of wave group W
 };
 template <int MODE> struct StripThreads { static constexpr int value = MODE == kPair64 ? 512 : 256; };
 
-template <int SS, int TRB, int MODE, int W>
+// PH (stride 2): the strided correlation is run as a stride-1 one over the
+// four phase images x[ci][2i + pr][2j + pc]: phase channel c' = 4 ci + 2 pr
+// + pc, phase taps (r', s') with r = 2 r' + pr, s = 2 s' + pc (Eq. (2) with
+// the sum over the filter split by the parity of r and s).  Staging loads
+// the two x rows of a phase row and keeps every other column; SS and TRB are
+// then the phase filter's width and height.
+template <int SS, int TRB, int MODE, int W, bool PH = false>
 __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* smem) {
     constexpr int CB = MODE == kTapSplit ? 32 : 64;         // channels / filters staged
     constexpr int NTH = StripThreads<MODE>::value;
@@ -214,7 +230,8 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
     const int q0 = qb * kBQ;
     const int r0 = blockIdx.y * TRB;
     constexpr int nTR = TRB;                      // the plan makes every row group full
-    const int ncsb = (a.C + CB - 1) / CB;
+    const int Cst = PH ? 4 * a.C : a.C;           // channels of the staged image
+    const int ncsb = (Cst + CB - 1) / CB;
     const int o0 = (blockIdx.z / ncsb) * CB, c0 = (blockIdx.z % ncsb) * CB;
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -228,10 +245,10 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
                           int64_t(n) * a.K * dy_rows * a.dy_pitch;
     const int64_t xplane = int64_t(a.x_rows) * a.x_pitch;
     const int64_t dyplane = int64_t(dy_rows) * a.dy_pitch;
-    const int xg0 = q0 + a.base_c;                 // global column of staged x column 0
+    const int xg0 = (PH ? 2 * q0 : q0) + a.base_c; // global column of staged x column 0
     const int dyg0 = q0 + a.dy_off;                // global column of staged dy column 0
     const int dy_end = a.dy_off + a.Wot;           // dy interior ends here
-    const int xrow0 = p0 + a.base_r + r0;          // x row of ring row 0
+    const int xrow0 = PH ? p0 + r0 : p0 + a.base_r + r0;   // x row (PH: phase row) of ring row 0
     const int dysh = dyg0 & 7, dya0 = dyg0 - dysh;
 
     // staging units: x row = CB channels x 9 groups of 8; dy row = CB filters x 8 groups
@@ -247,23 +264,56 @@ __device__ __forceinline__ void strip_body(const WgradArgs& a, unsigned char* sm
     // step j-1; buffer j % kDepth holds it.
     struct Regs {
         uint4 x[XPT];
+        uint4 x2[PH ? XPT : 1];   // PH: the next 8 columns (a phase row needs 16 x columns per 8)
         uint4 d0[DPT], d1[DPT];
     };
     Regs buf[kDepth];
 
     auto load_x = [&](int m, Regs& r) {   // ring row m -> registers
-        const int gr = min(max(xrow0 + m, 0), a.x_rows - 1);
 #pragma unroll
         for (int k = 0; k < XPT; ++k) {
             const int u = min(tid + k * NTH, XU - 1);
             const int ci = u / 9, g8 = u - ci * 9;
-            const int gc = min(xg0 + 8 * g8, a.x_pitch - 8);
-            r.x[k] = *reinterpret_cast<const uint4*>(xt + min(c0 + ci, a.C - 1) * xplane +
-                                                     int64_t(gr) * a.x_pitch + gc);
+            if constexpr (PH) {
+                const int cp = min(c0 + ci, Cst - 1), pr = (cp >> 1) & 1;
+                const int gr = min(max(2 * (xrow0 + m) + pr + a.base_r, 0), a.x_rows - 1);
+                const uint16_t* row = xt + (cp >> 2) * xplane + int64_t(gr) * a.x_pitch;
+                r.x[k] = *reinterpret_cast<const uint4*>(row + min(xg0 + 16 * g8, a.x_pitch - 8));
+                r.x2[k] = *reinterpret_cast<const uint4*>(row + min(xg0 + 16 * g8 + 8, a.x_pitch - 8));
+            } else {
+                const int gr = min(max(xrow0 + m, 0), a.x_rows - 1);
+                const int gc = min(xg0 + 8 * g8, a.x_pitch - 8);
+                r.x[k] = *reinterpret_cast<const uint4*>(xt + min(c0 + ci, a.C - 1) * xplane +
+                                                         int64_t(gr) * a.x_pitch + gc);
+            }
         }
     };
     auto store_x = [&](int m, Regs& r) {
         uint16_t* slot = xring + (m % NR) * CB * kXP;
+        if constexpr (PH) {
+            // columns 2j + pc of the two loaded chunks; zero outside the tile
+#pragma unroll
+            for (int k = 0; k < XPT; ++k) {
+                const int u = min(tid + k * NTH, XU - 1);
+                const int ci = u / 9, g8 = u - ci * 9;
+                const int cp = c0 + ci, pr = (cp >> 1) & 1, pc = cp & 1;
+                const int gr = 2 * (xrow0 + m) + pr + a.base_r;
+                const int col = xg0 + 16 * g8 + pc;   // x column of element 0
+                const int nv = (gr >= 0 && gr < a.x_rows && cp < Cst && col < a.x_cols)
+                                   ? (a.x_cols - col + 1) / 2 : 0;
+                const uint32_t sw[8] = {r.x[k].x, r.x[k].y, r.x[k].z, r.x[k].w,
+                                        r.x2[k].x, r.x2[k].y, r.x2[k].z, r.x2[k].w};
+                uint32_t o[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    o[j] = pc ? ((sw[2 * j] >> 16) | (sw[2 * j + 1] & 0xffff0000u))
+                              : ((sw[2 * j] & 0xffffu) | (sw[2 * j + 1] << 16));
+                if (NT > 1 || tid + k * NTH < XU)
+                    *reinterpret_cast<uint4*>(slot + ci * kXP + 8 * g8) =
+                        mask8(make_uint4(o[0], o[1], o[2], o[3]), nv);
+            }
+            return;
+        }
         const int gr = xrow0 + m;
         const bool rok = gr >= 0 && gr < a.x_rows;
         // With several taps the staging stays branch-free, so that it can sit
@@ -468,6 +518,19 @@ __global__ __launch_bounds__(512) void wgrad_pair_bf16_kernel(WgradArgs a) {
         strip_body<SS, TRB, kPair64, 0>(a, smem);
     else
         strip_body<SS, TRB, kPair64, 1>(a, smem);
+}
+
+// stride 2, at most 8 channels (32 phase channels): the tap-split kernel on
+// the phase images
+template <int SS, int TRB>
+__global__ __launch_bounds__(kThreads) void wgrad_taps2_bf16_kernel(WgradArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    switch (threadIdx.x >> 6) {
+        case 0: strip_body<SS, TRB, kTapSplit, 0, true>(a, smem); break;
+        case 1: strip_body<SS, TRB, kTapSplit, 1, true>(a, smem); break;
+        case 2: strip_body<SS, TRB, kTapSplit, 2, true>(a, smem); break;
+        default: strip_body<SS, TRB, kTapSplit, 3, true>(a, smem); break;
+    }
 }
 
 template <int SS, int TRB>
@@ -762,7 +825,21 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
     const int l = threadIdx.x;
     const float total = ((red[0][l] + red[1][l]) + red[2][l]) + red[3][l];
     int64_t idx;
-    if (a.frag == 2) {
+    if (a.frag == 3) {
+        // phase images: [gy][gz][phase tap][16][64], 32x32 blocks of (filter,
+        // phase channel 4 ci + 2 pr + pc); tap (r', s') is filter tap (2r' + pr, 2s' + pc)
+        const int SP = (a.S + 1) / 2, NT = a.TRB * SP;
+        int64_t t = f;
+        const int lane = int(t % 64); t /= 64;
+        const int e = int(t % 16); t /= 16;
+        const int tap = int(t % NT); t /= NT;
+        const int bz = int(t % a.gz);
+        const int o = bz * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
+        const int cp = lane & 31, ci = cp >> 2;
+        const int r = 2 * (tap / SP) + ((cp >> 1) & 1), s = 2 * (tap % SP) + (cp & 1);
+        if (r >= a.R || s >= a.S || o >= a.K || ci >= a.C) return;
+        idx = ((int64_t(o) * a.C + ci) * a.R + r) * a.S + s;
+    } else if (a.frag == 2) {
         // [gy][gz][tap][16][64] -> (o, ci, r, s), 32x32 blocks
         const int NT = a.TRB * a.S;
         int64_t t = f;
@@ -824,6 +901,14 @@ static hipError_t launch_strip(const WgradArgs& a, dim3 grid, hipStream_t s) {
 }
 
 template <int SS>
+static hipError_t launch_taps2(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    hipError_t e = set_lds(wgrad_taps2_bf16_kernel<SS, SS>, a.lds_bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((wgrad_taps2_bf16_kernel<SS, SS>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
+template <int SS>
 static hipError_t launch_taps(const WgradArgs& a, dim3 grid, hipStream_t s) {
     hipError_t e = set_lds(wgrad_taps_bf16_kernel<SS, SS>, a.lds_bytes);
     if (e != hipSuccess) return e;
@@ -853,6 +938,13 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
         DC_STRIP(5, 1) DC_STRIP(6, 1) DC_STRIP(7, 1)
         return hipErrorInvalidValue;
 #undef DC_STRIP
+    } else if (a.kind == WGRAD_TAPS2_BF16) {
+        switch ((a.S + 1) / 2) {
+            case 2: e = launch_taps2<2>(a, grid, s); break;
+            case 3: e = launch_taps2<3>(a, grid, s); break;
+            case 4: e = launch_taps2<4>(a, grid, s); break;
+            default: return hipErrorInvalidValue;
+        }
     } else if (a.kind == WGRAD_TAPS_BF16) {
         switch (a.S) {
             case 2: e = launch_taps<2>(a, grid, s); break;

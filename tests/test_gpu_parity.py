@@ -90,6 +90,9 @@ SMALL = {
     "taps3_bf16": Layer("taps3_bf16", 2, 16, 24, 40, 40, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 91),
     "taps5_bf16": Layer("taps5_bf16", 2, 32, 20, 36, 52, 5, 5, 1, 2, 2, 2, 2, "bf16", "uniform", 92),
     "taps7_bf16": Layer("taps7_bf16", 1, 8, 32, 48, 48, 7, 7, 1, 3, 2, 2, 3, "bf16", "uniform", 93),
+    # stride 2 with at most 8 channels: the weight gradient on the four phase
+    # images (partial filter block, partial strips, decomposed)
+    "s2taps_bf16": Layer("s2taps_bf16", 2, 5, 40, 36, 52, 5, 5, 2, 2, 2, 2, 2, "bf16", "uniform", 94),
 }
 
 
@@ -138,7 +141,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
-                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16"])
+                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
