@@ -292,6 +292,7 @@ static int lds_bytes_for(const IgemmArgs& a, int dtype, int CC, int OB) {
 bool igemm_plan(IgemmArgs& a, int dtype) {
     a.kind = 0;
     if (dtype == 1 && igemm_wreg_plan(a)) return true;
+    if (dtype == 0 && igemm_f32w_plan(a)) return true;
     a.OB = a.Cout <= 32 ? 32 : 64;
     // channel-chunk candidates, widest first: the channel count itself (rounded
     // to the k-granularity) when it is small, then powers of two
@@ -319,6 +320,7 @@ bool igemm_plan(IgemmArgs& a, int dtype) {
 
 hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
     if (a.kind == 1) return launch_igemm_wreg(a, s);
+    if (a.kind == 2) return launch_igemm_f32w(a, s);
     const int nvb = (a.Vo + kBW - 1) / kBW, nub = (a.Uo + kBH - 1) / kBH;
     dim3 grid(nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
     dim3 block(kThreads);

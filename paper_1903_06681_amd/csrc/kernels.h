@@ -63,7 +63,7 @@ struct IgemmArgs {
     int CC;                      // channels per LDS chunk (multiple of 8 for bf16, 2 for fp32)
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
-    int kind;                    // 0: chunked kernel; 1: register-weight strip kernel
+    int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32)
     int nvb, nseg, rows_per_seg; // strip kernel: 64-column strips, row segments
 };
 
@@ -75,6 +75,8 @@ bool igemm_plan(IgemmArgs& a, int dtype);
 hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s);
 bool igemm_wreg_plan(IgemmArgs& a);
 hipError_t launch_igemm_wreg(const IgemmArgs& a, hipStream_t s);
+bool igemm_f32w_plan(IgemmArgs& a);
+hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s);
 
 // ----------------------------------------------------- weight gradient
 //
