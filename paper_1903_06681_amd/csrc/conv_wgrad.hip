@@ -72,6 +72,20 @@ struct Plan {
 // the accumulators (at most 14 tiles of 32x32 per wave)
 static bool taps_filter(int R, int S) { return R == S && R >= 2 && R <= 7; }
 
+// fp32 flattened-column kernel: instantiated (C, R, S)
+static bool f32w_shape(int C, int R, int S) {
+    const int shapes[][3] = {{18, 3, 3}, {4, 3, 3}, {8, 3, 3}, {5, 3, 3}, {6, 1, 1}, {16, 3, 3}};
+    for (auto& s : shapes)
+        if (s[0] == C && s[1] == R && s[2] == S) return true;
+    return false;
+}
+static int f32w_lds(int C, int R, int S) {
+    const int XW = 64 + S - 1 + 3, XWP = (XW + 3) / 4 * 4 + 4, DYP = 17 * 4 + 4;
+    const int ring = ((R + 1) * C * XWP + 2 * 32 * DYP) * 4;
+    const int red = 4 * ((C * R * S + 31) / 32) * 1024 * 4;
+    return ring > red ? ring : red;
+}
+
 static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, int stride,
                       int Hot, int Wot, int base_c, Plan* pl) {
     std::memset(pl, 0, sizeof(*pl));
@@ -116,6 +130,22 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
         pl->F = int64_t(pl->gy) * pl->gz * (pl->frag == 1 ? 4 : 1) * pl->TRB * SP * 1024;
         return true;
     }
+    if (dtype == 0 && stride == 1 && f32w_shape(C, R, S)) {
+        pl->kind = WGRAD_F32W;
+        pl->TRB = R;
+        pl->gy = 1;
+        pl->gz = (K + 31) / 32;
+        pl->nqb = (Wot + kBQ - 1) / kBQ;
+        const int strips = ntiles * N * pl->nqb;
+        const int want = std::max(1, kTargetWGs / pl->gz);
+        int nseg = std::max(1, std::min(Hot, (want + strips - 1) / strips));
+        pl->rows_per_seg = (Hot + nseg - 1) / nseg;
+        pl->nseg = (Hot + pl->rows_per_seg - 1) / pl->rows_per_seg;
+        pl->nchunks = strips * pl->nseg;
+        pl->F = int64_t(pl->gz) * ((C * R * S + 31) / 32) * 1024;
+        pl->frag = 4;
+        return true;
+    }
     if (dtype == 1) {
         if (S > 7) return false;
         pl->kind = WGRAD_ROWS_BF16;
@@ -155,7 +185,9 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
     a.chunks_per_tile = pl.chunks_per_tile; a.rows_per_chunk = pl.rows_per_chunk;
     a.nqb = pl.nqb; a.nseg = pl.nseg; a.rows_per_seg = pl.rows_per_seg;
     a.F = pl.F; a.frag = pl.frag;
-    if (a.kind == WGRAD_STRIP_BF16 || a.kind == WGRAD_TAPS_BF16 || a.kind == WGRAD_TAPS2_BF16) {
+    if (a.kind == WGRAD_F32W) {
+        a.lds_bytes = f32w_lds(a.C, a.R, a.S);
+    } else if (a.kind == WGRAD_STRIP_BF16 || a.kind == WGRAD_TAPS_BF16 || a.kind == WGRAD_TAPS2_BF16) {
         const int cb = a.kind == WGRAD_STRIP_BF16 ? 64 : 32;
         a.lds_bytes = ((a.TRB + 1) * cb * kXP + 2 * cb * kXP) * 2;
     } else if (a.kind == WGRAD_ROWS_BF16) {
@@ -795,6 +827,172 @@ __global__ __launch_bounds__(kThreads) void wgrad_rows_f32_kernel(WgradArgs a) {
     }
 }
 
+
+// ---------------------------------------------------------------- fp32, columns in registers
+
+// fp32 stride 1 with few flattened columns (C*R*S <= 256): v_mfma_f32_32x32x2_f32
+// with rows = 32 filters, columns = 32 flattened (ci, r, s), a k-step = two
+// output pixels.  A workgroup walks down a 64-column strip; each wave owns 16
+// pixels of every row (8 k-steps) and keeps all NB column blocks in
+// accumulators; A (dy) and B (x) are single 4-byte LDS reads at per-lane
+// offsets (rows are staged from aligned 16-byte chunks; the misalignment is
+// absorbed in the read offset).  The four waves' sums are added in LDS at
+// the end (fixed order) and written as one partial in fragment order.
+namespace {
+typedef float f32x4w __attribute__((ext_vector_type(4)));
+template <int S_> struct F32WgGeom {
+    static constexpr int XW = 64 + S_ - 1 + 3;             // staged x columns (+3: alignment shift)
+    static constexpr int XV = (XW + 3) / 4;                // 16-byte units per staged x row
+    static constexpr int XWP = XV * 4 + 4;                 // x row pitch (floats)
+    static constexpr int DV = 17;                          // 16-byte units per staged dy row (64 + 3)
+    static constexpr int DYP = DV * 4 + 4;                 // dy row pitch (floats)
+};
+}  // namespace
+
+template <int CIN, int RR, int SS>
+__global__ __launch_bounds__(kThreads, 1) void wgrad_f32w_kernel(WgradArgs a) {
+    using G = F32WgGeom<SS>;
+    constexpr int CRS = CIN * RR * SS, NB = (CRS + 31) / 32;
+    constexpr int NRX = RR + 1;                             // x ring slots
+    constexpr int XSL = CIN * G::XWP;                       // floats per x slot
+    constexpr int XUN = CIN * G::XV, DUN = 32 * G::DV;      // 16-byte units per x / dy row
+    constexpr int XPT = (XUN + kThreads - 1) / kThreads, DPT = (DUN + kThreads - 1) / kThreads;
+    extern __shared__ __align__(16) unsigned char smem[];
+    float* xring = reinterpret_cast<float*>(smem);          // [NRX][CIN][XWP]
+    float* dyb = xring + NRX * XSL;                         // [2][32][DYP]
+
+    int c = blockIdx.x;
+    const int seg = c % a.nseg; c /= a.nseg;
+    const int qb = c % a.nqb; c /= a.nqb;
+    const int n = c % a.Nn;
+    const int tile = c / a.Nn;
+    const int p0 = seg * a.rows_per_seg;
+    const int nrows = min(a.rows_per_seg, a.Hot - p0);
+    const int q0 = qb * kBQ;
+    const int o0 = blockIdx.z * 32;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int l32 = lane & 31, hi = lane >> 5;
+
+    const float* xt = static_cast<const float*>(a.x) + tile * a.x_tile +
+                      int64_t(n) * a.C * a.x_rows * a.x_pitch;
+    const int dy_rows = a.Hot + 2 * a.dy_off;
+    const float* dyt = static_cast<const float*>(a.dy) + tile * a.dy_tile +
+                       int64_t(n) * a.K * dy_rows * a.dy_pitch;
+    const int64_t xplane = int64_t(a.x_rows) * a.x_pitch;
+    const int64_t dyplane = int64_t(dy_rows) * a.dy_pitch;
+    const int xg = q0 + a.base_c, xa = xg & ~3, xsh = xg - xa;           // x column of pixel 0
+    const int dg = q0 + a.dy_off, da = dg & ~3, dsh = dg - da;           // dy column of pixel 0
+    const int dy_end = a.dy_off + a.Wot;
+    const int xrow0 = p0 + a.base_r;
+
+    f32x4w xs[XPT], ds[DPT];
+    auto load_x = [&](int m) {   // ring row m (x row xrow0 + m) -> registers
+        const int gr = min(max(xrow0 + m, 0), a.x_rows - 1);
+        static_for<0, XPT>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            const int u = min(tid + k * kThreads, XUN - 1);
+            const int ci = u / G::XV, g = u % G::XV;
+            xs[k] = *reinterpret_cast<const f32x4w*>(xt + ci * xplane + int64_t(gr) * a.x_pitch +
+                                                     min(xa + 4 * g, a.x_pitch - 4));
+        });
+    };
+    auto store_x = [&](int m) {   // zero outside the tile: padding columns feed masked pixels
+        float* slot = xring + (m % NRX) * XSL;
+        static_for<0, XPT>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            const int u = min(tid + k * kThreads, XUN - 1);
+            const int ci = u / G::XV, g = u % G::XV;
+            const int col = xa + 4 * g;
+            f32x4w v = xs[k];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = col + e < a.x_cols ? v[e] : 0.f;
+            *reinterpret_cast<f32x4w*>(slot + ci * G::XWP + 4 * g) = v;
+        });
+    };
+    auto load_dy = [&](int i) {   // output row p0 + i -> registers (clamped)
+        const int gr = min(p0 + i + a.dy_off, dy_rows - 1);
+        static_for<0, DPT>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            const int u = min(tid + k * kThreads, DUN - 1);
+            const int o = u / G::DV, g = u % G::DV;
+            ds[k] = *reinterpret_cast<const f32x4w*>(dyt + min(o0 + o, a.K - 1) * dyplane +
+                                                     int64_t(gr) * a.dy_pitch + min(da + 4 * g, a.dy_pitch - 4));
+        });
+    };
+    auto store_dy = [&](int i) {  // only the interior of filters < K: other pixels add zero
+        float* slot = dyb + (i & 1) * 32 * G::DYP;
+        static_for<0, DPT>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            const int u = min(tid + k * kThreads, DUN - 1);
+            const int o = u / G::DV, g = u % G::DV;
+            const int col = da + 4 * g;
+            f32x4w v = ds[k];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] = (o0 + o < a.K && col + e >= dg && col + e < dy_end) ? v[e] : 0.f;
+            *reinterpret_cast<f32x4w*>(slot + o * G::DYP + 4 * g) = v;
+        });
+    };
+
+    // per-lane column (ci, r, s) of each block: x offset inside a slot and filter row
+    int boff[NB], brow[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        const int col = min(32 * b + l32, CRS - 1);   // columns past CRS are never stored
+        const int ci = col / (RR * SS), r = (col / SS) % RR, sx = col % SS;
+        boff[b] = ci * G::XWP + xsh + sx;
+        brow[b] = r;
+    }
+    floatx16 acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
+
+    for (int m = 0; m < RR; ++m) {
+        load_x(m);
+        store_x(m);
+    }
+    load_dy(0);
+    store_dy(0);
+    __syncthreads();
+
+    const int pw = 16 * wave + hi;   // this lane's first pixel; k-step k adds 2k
+    for (int i = 0; i < nrows; ++i) {
+        load_x(i + RR);
+        load_dy(i + 1);
+        const float* arow = dyb + (i & 1) * 32 * G::DYP + l32 * G::DYP + dsh + pw;
+        const float* bsl[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) bsl[b] = xring + ((i + brow[b]) % NRX) * XSL + boff[b] + pw;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const float av = arow[2 * k];
+            float bv[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) bv[b] = bsl[b][2 * k];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv[b], acc[b], 0, 0, 0);
+        }
+        // x slot (i + RR) % NRX and dy buffer (i + 1) & 1 were last read in step i - 1
+        store_x(i + RR);
+        store_dy(i + 1);
+        __syncthreads();
+    }
+
+    // the four waves' sums, added in wave order in LDS, one partial per chunk:
+    // [chunk][gz][block][16][64] in fragment order
+    float* red = xring;   // the ring is free now: 4 x NB x 1024 floats
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) red[((wave * NB + b) * 16 + e) * 64 + lane] = acc[b][e];
+    __syncthreads();
+    float* part = a.part + int64_t(blockIdx.x) * a.F + int64_t(blockIdx.z) * NB * 1024;
+    for (int f = tid; f < NB * 1024; f += kThreads)
+        part[f] = ((red[f] + red[NB * 1024 + f]) + red[2 * NB * 1024 + f]) + red[3 * NB * 1024 + f];
+}
+
 // ---------------------------------------------------------------- reduction
 
 // dw = (accumulate ? dw : 0) + sum over chunks of the partials, in a fixed
@@ -825,7 +1023,19 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
     const int l = threadIdx.x;
     const float total = ((red[0][l] + red[1][l]) + red[2][l]) + red[3][l];
     int64_t idx;
-    if (a.frag == 3) {
+    if (a.frag == 4) {
+        // fp32 flattened columns: [gz][block][16][64], rows = filters, columns = (ci, r, s)
+        const int NB = (a.C * a.R * a.S + 31) / 32;
+        int64_t t = f;
+        const int lane = int(t % 64); t /= 64;
+        const int e = int(t % 16); t /= 16;
+        const int b = int(t % NB); t /= NB;
+        const int bz = int(t);
+        const int o = bz * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
+        const int col = 32 * b + (lane & 31);
+        if (o >= a.K || col >= a.C * a.R * a.S) return;
+        idx = int64_t(o) * a.C * a.R * a.S + col;
+    } else if (a.frag == 3) {
         // phase images: [gy][gz][phase tap][16][64], 32x32 blocks of (filter,
         // phase channel 4 ci + 2 pr + pc); tap (r', s') is filter tap (2r' + pr, 2s' + pc)
         const int SP = (a.S + 1) / 2, NT = a.TRB * SP;
@@ -900,6 +1110,14 @@ static hipError_t launch_strip(const WgradArgs& a, dim3 grid, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int C_, int R_, int S_>
+static hipError_t launch_f32wg(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    hipError_t e = set_lds(wgrad_f32w_kernel<C_, R_, S_>, a.lds_bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((wgrad_f32w_kernel<C_, R_, S_>), grid, dim3(kThreads), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
 template <int SS>
 static hipError_t launch_taps2(const WgradArgs& a, dim3 grid, hipStream_t s) {
     hipError_t e = set_lds(wgrad_taps2_bf16_kernel<SS, SS>, a.lds_bytes);
@@ -938,6 +1156,13 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
         DC_STRIP(5, 1) DC_STRIP(6, 1) DC_STRIP(7, 1)
         return hipErrorInvalidValue;
 #undef DC_STRIP
+    } else if (a.kind == WGRAD_F32W) {
+#define DC_F32WG(c, r, s_) \
+        if (a.C == c && a.R == r && a.S == s_) e = launch_f32wg<c, r, s_>(a, grid, s); else
+        DC_F32WG(18, 3, 3) DC_F32WG(4, 3, 3) DC_F32WG(8, 3, 3) DC_F32WG(5, 3, 3) DC_F32WG(6, 1, 1)
+        DC_F32WG(16, 3, 3)
+        return hipErrorInvalidValue;
+#undef DC_F32WG
     } else if (a.kind == WGRAD_TAPS2_BF16) {
         switch ((a.S + 1) / 2) {
             case 2: e = launch_taps2<2>(a, grid, s); break;

@@ -87,7 +87,7 @@ hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s);
 // summed over the chunk's (n, p, q).
 
 enum WgradKind { WGRAD_STRIP_BF16 = 0, WGRAD_ROWS_BF16 = 1, WGRAD_ROWS_F32 = 2, WGRAD_TAPS_BF16 = 3,
-                 WGRAD_TAPS2_BF16 = 4 };
+                 WGRAD_TAPS2_BF16 = 4, WGRAD_F32W = 5 };
 
 struct WgradArgs {
     const void* x;               // padded x tiles
@@ -111,8 +111,9 @@ struct WgradArgs {
     int chunks_per_tile, rows_per_chunk;   // row kinds: flattened (n, p) rows per chunk
     int nqb, nseg, rows_per_seg;           // strip kind: 64-column strips, row segments
     int64_t F;                   // floats per chunk partial
-    int frag;                    // 0: partials in dw order; 1, 2, 3: in MFMA fragment order
-                                 // (64x64 blocks, 32x32 blocks, 32x32 blocks of stride-2 phase images)
+    int frag;                    // 0: partials in dw order; 1 .. 4: in MFMA fragment order (64x64
+                                 // blocks, 32x32 blocks, 32x32 blocks of stride-2 phase images,
+                                 // fp32 32 filters x 32 flattened (ci, r, s))
     int lds_bytes;
 };
 
