@@ -171,6 +171,54 @@ def cpu_baseline(L, x, w, dy, tile, seconds):
     }
 
 
+def all_workloads(steps):
+    """Per-pass times of every workload's single-tile configuration (inputs
+    of constant value: the time does not depend on them), each pass K times
+    back to back between two events on the launch stream."""
+    import torch
+    import harness as H
+    import paper_1903_06681_amd as dc
+    import workloads as wl
+
+    res = {}
+    stream = torch.cuda.current_stream()
+    for name, L in wl.LAYERS.items():
+        p = dc.Problem.of(L)
+        tile = L.tiles[0] if L.tiles else 0
+        xp = H.alloc_tiles(p, dc.DC_X, 1, L.dtype, fill=0.5)[0]
+        dyp = H.alloc_tiles(p, dc.DC_DY, 1, L.dtype, fill=0.25)[0]
+        w = torch.full((L.K, L.C, L.R, L.S), 0.125, dtype=H.TORCH_DT[L.dtype], device="cuda")
+        y = torch.empty((L.N, L.K, L.Hot, L.Wot), device="cuda")
+        dx = torch.empty((L.N, L.C, L.Ht, L.Wt), device="cuda")
+        dw = torch.empty((L.K, L.C, L.R, L.S), device="cuda")
+        ws = torch.empty(max(dc.bwd_filter_workspace_bytes(p, tile), 16), dtype=torch.uint8, device="cuda")
+        calls = {"fwd": lambda: dc.conv_fwd(p, tile, xp, w, y),
+                 "bwd_data": lambda: dc.conv_bwd_data(p, tile, dyp, w, dx),
+                 "bwd_filter": lambda: dc.conv_bwd_filter(p, tile, xp, dyp, dw, 0, ws)}
+        alg = algorithmic(L)
+        peak = PEAK["bf16_tflops"] if L.dtype == "bf16" else PEAK["f32_tflops"]
+        d = {"desc": L.desc, "tile": tile}
+        for k, f in calls.items():
+            for _ in range(3):
+                f()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(steps):
+                f()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            a = alg[k]
+            roof = min(peak, a["flops"] / a["bytes"] * PEAK["hbm_gbps"] / 1e3)
+            tf = a["flops"] / (ms * 1e-3) / 1e12
+            d[k] = {"ms": round(ms, 5), "TFLOP/s": round(tf, 2), "roof_TFLOP/s": round(roof, 1),
+                    "pct_roof": round(100 * tf / roof, 2)}
+        res[name] = d
+        del xp, dyp, y, dx, ws
+    return res
+
+
 def copy_calibration(mib):
     """dst = src * 1 over MIB MiB of fp32: reads and writes exactly MIB MiB each."""
     import torch
@@ -195,6 +243,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=24.0)
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the cold timings (each step or pass after a 512 MB cache flush)")
+    ap.add_argument("--all-workloads", action="store_true",
+                    help="also time every workload's single-tile passes (field 'workloads')")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB a few times (the known-size "
                          "kernel against which HBM byte counters are scaled) and exit")
@@ -451,6 +501,8 @@ def main():
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, x, w, dy, tile, args.cpu_seconds)
+    if args.all_workloads:
+        out["workloads"] = all_workloads(args.steps)
     print(json.dumps(out), flush=True)
 
 
