@@ -39,7 +39,14 @@ __device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[
         }
 }
 
-template <int NOB, int TR, int TS, int CG, int MINWG>
+// PH (forward at stride 2 with at most 4 channels): the strided correlation
+// of Eq. (1) as a stride-1 one over the four phase images x[ci][2i + pr][2j +
+// pc], phase channel c' = 4 ci + 2 pr + pc (padded to 16 with zero weights),
+// phase taps (r', s') = filter tap (2r' + pr, 2s' + pc); TR x TS is then the
+// phase filter.  Ring row m holds phase row u0 + m: each staging block loads
+// the two 16-byte chunks of four (ci, pr) rows and keeps the columns of one
+// parity per phase channel.
+template <int NOB, int TR, int TS, int CG, int MINWG, bool PH = false>
 __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs a) {
     constexpr int KS = TR * TS * CG;          // 16-wide k-steps: (tap, 16-channel group)
     constexpr int CIN = CG * 16;
@@ -76,8 +83,8 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
     const uint16_t* in = static_cast<const uint16_t*>(a.in) + tile * a.in_tile +
                          int64_t(n) * a.Cin * plane;
-    const int xr0 = u0 + a.base_r;   // input row of ring row 0 (stride-1 walk)
-    const int xc0 = v0 + a.base_c;   // input column of staged pixel 0 (a multiple of 8)
+    const int xr0 = PH ? u0 : u0 + a.base_r;       // input row (PH: phase row) of ring row 0
+    const int xc0 = (PH ? 2 * v0 : v0) + a.base_c; // input column of staged pixel 0 (a multiple of 8)
     uint4 stg[BPT][8], stg1[BPT][8];
 
     auto load_rows = [&](uint4 (&sg)[BPT][8], int m0, int nrow) {   // ring rows m0 .. m0+nrow-1 -> registers
@@ -90,12 +97,26 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 // Unconditional 16-byte loads from clamped addresses: a row or
                 // column outside the tile only ever feeds output pixels that
                 // are not stored, so its values need no masking.
-                const int gr = min(max(xr0 + m, 0), a.in_rows - 1);
-                const int gc = min(xc0 + pg * 8, a.in_pitch - 8);
-                const uint16_t* src = in + int64_t(gr) * a.in_pitch + gc + (cg8 * 8) * plane;
+                if constexpr (PH) {
+                    // phase channels 8 cg8 .. + 7 = four (ci, pr) rows x two parities
+                    const int gc = min(xc0 + pg * 16, a.in_pitch - 8);
+                    const int gc2 = min(xc0 + pg * 16 + 8, a.in_pitch - 8);
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    sg[b][j] = *reinterpret_cast<const uint4*>(src + j * plane);
+                    for (int q = 0; q < 4; ++q) {
+                        const int cpq = cg8 * 8 + 2 * q, ci = min(cpq >> 2, a.Cin - 1), pr = (cpq >> 1) & 1;
+                        const int gr = min(max(2 * (xr0 + m) + pr + a.base_r, 0), a.in_rows - 1);
+                        const uint16_t* src = in + int64_t(ci) * plane + int64_t(gr) * a.in_pitch;
+                        sg[b][2 * q] = *reinterpret_cast<const uint4*>(src + gc);
+                        sg[b][2 * q + 1] = *reinterpret_cast<const uint4*>(src + gc2);
+                    }
+                } else {
+                    const int gr = min(max(xr0 + m, 0), a.in_rows - 1);
+                    const int gc = min(xc0 + pg * 8, a.in_pitch - 8);
+                    const uint16_t* src = in + int64_t(gr) * a.in_pitch + gc + (cg8 * 8) * plane;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        sg[b][j] = *reinterpret_cast<const uint4*>(src + j * plane);
+                }
             }
         }
     };
@@ -107,7 +128,27 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
                 const int m = m0 + blk / BLK_ROW, rb = blk % BLK_ROW;
                 const int cg8 = rb % NCG8, pg = rb / NCG8;
                 uint4 t[8];
-                transpose8x8(sg[b], t);
+                if constexpr (PH) {
+                    // channel 2q + pc: columns of parity pc of the q-th row's 16
+                    uint4 ch[8];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t w8[8] = {sg[b][2 * q].x, sg[b][2 * q].y, sg[b][2 * q].z, sg[b][2 * q].w,
+                                                sg[b][2 * q + 1].x, sg[b][2 * q + 1].y,
+                                                sg[b][2 * q + 1].z, sg[b][2 * q + 1].w};
+                        uint32_t e[4], o[4];
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            e[k] = (w8[2 * k] & 0xffffu) | (w8[2 * k + 1] << 16);
+                            o[k] = (w8[2 * k] >> 16) | (w8[2 * k + 1] & 0xffff0000u);
+                        }
+                        ch[2 * q] = make_uint4(e[0], e[1], e[2], e[3]);
+                        ch[2 * q + 1] = make_uint4(o[0], o[1], o[2], o[3]);
+                    }
+                    transpose8x8(ch, t);
+                } else {
+                    transpose8x8(sg[b], t);
+                }
                 uint16_t* dst = lds + (m % NRING) * ROWSZ + (pg * 8) * PS + cg8 * 8;
 #pragma unroll
                 for (int p = 0; p < 8; ++p) *reinterpret_cast<uint4*>(dst + p * PS) = t[p];
@@ -141,7 +182,17 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     uint16_t* Wl = lds;
     {
         const uint16_t* w = static_cast<const uint16_t*>(a.w);
-        if (a.wvec && a.wmode == 0) {
+        if constexpr (PH) {
+            // phase weights: Wl[o][c'][t'] = w[o0+o][ci][2r'+pr][2s'+pc], zero past
+            // the filter and for the padding channels
+            for (int e = tid; e < OBT * RL; e += kWThreads) {
+                const int o = e / RL, r_ = e % RL, cp = r_ / T, t = r_ % T;
+                const int ci = cp >> 2, r = 2 * (t / TS) + ((cp >> 1) & 1), sx = 2 * (t % TS) + (cp & 1);
+                const int oc = min(o0 + o, a.Cout - 1);
+                const bool ok = ci < a.wC && r < a.R && sx < a.S;
+                Wl[o * PW + r_] = ok ? w[(int64_t(oc) * a.wC + ci) * a.R * a.S + r * a.S + sx] : uint16_t(0);
+            }
+        } else if (a.wvec && a.wmode == 0) {
             // rows o0 .. o0+OBT-1 of w are consecutive: 16-byte chunks straight to
             // LDS, all of a thread's loads in flight at once (chunks of rows
             // past Cout re-read the last valid chunk).  Every workgroup reads
@@ -387,7 +438,44 @@ static int wreg_lds(int NOB, int TR, int TS, int CG) {
     return ring > wl ? ring : wl;
 }
 
+// the phase-image forward (stride 2, at most 4 channels): instantiated
+// (NOB, phase filter) shapes
+static bool wreg_phase_shape(int NOB, int TR, int TS) {
+    return (NOB == 2 || NOB == 1) && ((TR == 4 && TS == 4) || (TR == 2 && TS == 2) || (TR == 3 && TS == 3));
+}
+
+static void wreg_segments(IgemmArgs& a) {
+    a.nvb = (a.Vo + 63) / 64;
+    const int strips = a.ntiles * a.Nn * a.nvb * ((a.Cout + a.OB - 1) / a.OB);
+    const int want = 256;
+    int nseg = (want + strips - 1) / strips;
+    nseg = nseg < 1 ? 1 : nseg;
+    int rps = (a.Uo + nseg - 1) / nseg;
+    rps = (rps + 1) & ~1;   // whole steps of two rows
+    if (rps < 2) rps = 2;
+    a.rows_per_seg = rps;
+    a.nseg = (a.Uo + rps - 1) / rps;
+}
+
 bool igemm_wreg_plan(IgemmArgs& a) {
+    a.phase = 0;
+    if (a.wmode == 0 && a.istr == 2 && a.ostr == 1 && 4 * a.Cin <= 16 && a.base_c % 8 == 0 &&
+        a.in_pitch % 8 == 0 && a.Tr == a.R && a.Ts == a.S) {
+        const int NOB = a.Cout <= 32 ? 1 : 2, TRp = (a.R + 1) / 2, TSp = (a.S + 1) / 2;
+        if (wreg_phase_shape(NOB, TRp, TSp)) {
+            const int lds = wreg_lds(NOB, TRp, TSp, 1);
+            if (lds <= device_lds_limit()) {
+                a.phase = 1;
+                a.Tr = TRp; a.Ts = TSp;
+                a.OB = NOB * 32;
+                a.wvec = 0;
+                wreg_segments(a);
+                a.lds_bytes = lds;
+                a.kind = 1;
+                return true;
+            }
+        }
+    }
     if (a.istr != 1 || a.Cin % 16 != 0 || a.Tr < 1 || a.Ts < 1) return false;
     if (a.base_c % 8 != 0 || a.in_pitch % 8 != 0) return false;   // 16-byte aligned row loads
     const int NOB = a.Cout <= 32 ? 1 : 2;
@@ -404,24 +492,15 @@ bool igemm_wreg_plan(IgemmArgs& a) {
     const int lds = wreg_lds(NOB, a.Tr, a.Ts, CG);
     if (lds > device_lds_limit()) return false;
     a.OB = NOB * 32;
-    a.nvb = (a.Vo + 63) / 64;
-    const int strips = a.ntiles * a.Nn * a.nvb * ((a.Cout + a.OB - 1) / a.OB);
-    const int want = 256;
-    int nseg = (want + strips - 1) / strips;
-    nseg = nseg < 1 ? 1 : nseg;
-    int rps = (a.Uo + nseg - 1) / nseg;
-    rps = (rps + 1) & ~1;   // whole steps of two rows
-    if (rps < 2) rps = 2;
-    a.rows_per_seg = rps;
-    a.nseg = (a.Uo + rps - 1) / rps;
+    wreg_segments(a);
     a.lds_bytes = lds;
     a.kind = 1;
     return true;
 }
 
-template <int NOB, int TR, int TS, int CG, int MINWG>
+template <int NOB, int TR, int TS, int CG, int MINWG, bool PH = false>
 static hipError_t launch_one(const IgemmArgs& a, hipStream_t s) {
-    auto k = igemm_wreg_kernel<NOB, TR, TS, CG, MINWG>;
+    auto k = igemm_wreg_kernel<NOB, TR, TS, CG, MINWG, PH>;
     if (a.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
@@ -434,6 +513,13 @@ static hipError_t launch_one(const IgemmArgs& a, hipStream_t s) {
 
 hipError_t launch_igemm_wreg(const IgemmArgs& a, hipStream_t s) {
     const int NOB = a.OB / 32, CG = a.Cin / 16;
+    if (a.phase) {
+#define DC_WREG_PH(nob, t) \
+        if (NOB == nob && a.Tr == t && a.Ts == t) return launch_one<nob, t, t, 1, 1, true>(a, s);
+        DC_WREG_PH(2, 4) DC_WREG_PH(1, 4) DC_WREG_PH(2, 2) DC_WREG_PH(1, 2) DC_WREG_PH(2, 3) DC_WREG_PH(1, 3)
+#undef DC_WREG_PH
+        return hipErrorInvalidValue;
+    }
 #define DC_WREG(nob, tr, ts, cg) \
     if (NOB == nob && a.Tr == tr && a.Ts == ts && CG == cg) \
         return launch_one<nob, tr, ts, cg, 1>(a, s);

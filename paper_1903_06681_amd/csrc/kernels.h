@@ -64,6 +64,7 @@ struct IgemmArgs {
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
     int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32)
+    int phase;                   // register-weight bf16 forward over the stride-2 phase images
     int nvb, nseg, rows_per_seg; // strip kernel: 64-column strips, row segments
 };
 

@@ -93,6 +93,9 @@ SMALL = {
     # stride 2 with at most 8 channels: the weight gradient on the four phase
     # images (partial filter block, partial strips, decomposed)
     "s2taps_bf16": Layer("s2taps_bf16", 2, 5, 40, 36, 52, 5, 5, 2, 2, 2, 2, 2, "bf16", "uniform", 94),
+    # stride 2 with at most 4 channels: the forward pass on the phase images
+    "s2ph5_bf16": Layer("s2ph5_bf16", 2, 4, 48, 36, 52, 5, 5, 2, 2, 2, 2, 2, "bf16", "uniform", 95),
+    "s2ph3_bf16": Layer("s2ph3_bf16", 2, 2, 24, 32, 32, 3, 3, 2, 1, 2, 2, 1, "bf16", "uniform", 96),
 }
 
 
@@ -141,7 +144,8 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
-                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16"])
+                                  "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16",
+                                  "s2ph5_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
