@@ -72,6 +72,37 @@ struct Plan {
 // the accumulators (at most 14 tiles of 32x32 per wave)
 static bool taps_filter(int R, int S) { return R == S && R >= 2 && R <= 7; }
 
+// k-slice kernel geometry (kernel below)
+template <int NW>
+struct KsliceGeom {
+    static constexpr int QW = 16 * NW;            // output columns per strip
+    static constexpr int XU8 = 2 * NW + 1;        // 16-byte chunks per staged row (QW + 8 columns)
+    static constexpr int P = 8 * XU8;             // staged row pitch (elements): rows 4 banks apart
+    static constexpr int NI = (32 * XU8 + 63) / 64;   // 64-chunk loads per staged block (x or dy)
+    static constexpr int REG = NI * 64 * 8;       // elements of a block's region (spare chunks at the end)
+    static constexpr int BUF = 2 * REG + 64 * 8;  // x region, dy region, 64 chunks nobody reads
+    static constexpr int LPW = (2 * NI + NW - 1) / NW;   // loads per wave per step
+    static constexpr int kDepth = 4;              // steps between a row's request and its use
+    static constexpr int loop_lds = (kDepth + 2) * BUF * 2;   // + the first two window rows (3-row filters)
+};
+
+// k-slice kernel: instantiated filters, and whether a sample's x and dy
+// planes are addressed with 32-bit byte offsets (a bound that holds for any
+// halo up to the tile size)
+static bool kslice_filter(int R, int S) { return R == 3 && S == 3; }
+static constexpr int kKsliceNW = 8;   // waves of the k-slice kernel (strip of 16 * NW columns)
+// layers whose staged elements all lie inside the tile: whole 32-blocks of
+// channels and filters, whole strips, halo at least the padding (x window
+// rows and columns inside the tile), dy columns at most one element past a
+// 16-byte boundary
+static bool kslice_layer(int C, int K, int R, int S, int Wot, int base_c, int dy_off) {
+    return kslice_filter(R, S) && C % 32 == 0 && K % 32 == 0 && Wot % (16 * kKsliceNW) == 0 &&
+           base_c >= 0 && base_c % 8 == 0 && (dy_off & 7) <= 1;
+}
+static bool kslice_offsets_fit(int C, int K, int R, int S, int Hot, int Wot) {
+    const int64_t rows = 3 * (int64_t(Hot) + R + 8), cols = 3 * (int64_t(Wot) + S + 16);
+    return 2 * int64_t(std::max(C, K)) * rows * cols < (int64_t(1) << 32);
+}
 // fp32 flattened-column kernel: instantiated (C, R, S)
 static bool f32w_shape(int C, int R, int S) {
     const int shapes[][3] = {{18, 3, 3}, {4, 3, 3}, {8, 3, 3}, {5, 3, 3}, {6, 1, 1}, {16, 3, 3}};
@@ -87,12 +118,13 @@ static int f32w_lds(int C, int R, int S) {
 }
 
 static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, int stride,
-                      int Hot, int Wot, int base_c, Plan* pl) {
+                      int Hot, int Wot, int base_c, int dy_off, Plan* pl) {
     std::memset(pl, 0, sizeof(*pl));
     const bool xcol_aligned = base_c % 8 == 0;   // strip staging reads whole 16-byte x chunks
     const bool phase2 = dtype == 1 && stride == 2 && 4 * C <= 32 && xcol_aligned &&
                         taps_filter((R + 1) / 2, (S + 1) / 2);
     if ((dtype == 1 && stride == 1 && S <= 7 && xcol_aligned) || phase2) {
+        int qw = kBQ;   // strip width
         if (phase2) {
             // the phase images: a stride-1 ceil(R/2) x ceil(S/2) filter on 4C channels
             pl->kind = WGRAD_TAPS2_BF16;
@@ -100,6 +132,15 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
             pl->gy = 1;
             pl->gz = (K + 31) / 32;
             pl->frag = 3;
+        } else if (kslice_layer(C, K, R, S, Wot, base_c, dy_off) &&
+                   kslice_offsets_fit(C, K, R, S, Hot, Wot)) {
+            // 32x32 blocks over strips of 16 * NW columns, every tap in one workgroup
+            pl->kind = WGRAD_KSLICE_BF16;
+            pl->TRB = R;
+            pl->gy = 1;
+            pl->gz = ((K + 31) / 32) * ((C + 31) / 32);
+            pl->frag = 5;
+            qw = 16 * kKsliceNW;
         } else if (C <= 32 && K <= 32 && taps_filter(R, S)) {
             // one 32x32 block, every tap in one row group: x and dy are read once
             pl->kind = WGRAD_TAPS_BF16;
@@ -119,7 +160,7 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
             pl->gz = ((K + 63) / 64) * ((C + 63) / 64);
             pl->frag = 1;
         }
-        pl->nqb = (Wot + kBQ - 1) / kBQ;
+        pl->nqb = (Wot + qw - 1) / qw;
         const int strips = ntiles * N * pl->nqb;
         const int want = std::max(1, kTargetWGs / (pl->gy * pl->gz));
         int nseg = std::max(1, std::min(Hot, (want + strips - 1) / strips));
@@ -171,15 +212,16 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
 }
 
 size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
-                             int stride, int Hot, int Wot, int base_c) {
+                             int stride, int Hot, int Wot, int base_c, int dy_off) {
     Plan pl;
-    if (!make_plan(dtype, ntiles, N, C, K, R, S, stride, Hot, Wot, base_c, &pl)) return 0;
+    if (!make_plan(dtype, ntiles, N, C, K, R, S, stride, Hot, Wot, base_c, dy_off, &pl)) return 0;
     return size_t(pl.nchunks) * size_t(pl.F) * sizeof(float);
 }
 
 bool wgrad_plan(WgradArgs& a, int dtype) {
     Plan pl;
-    if (!make_plan(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.istr, a.Hot, a.Wot, a.base_c, &pl))
+    if (!make_plan(dtype, a.ntiles, a.Nn, a.C, a.K, a.R, a.S, a.istr, a.Hot, a.Wot, a.base_c, a.dy_off,
+                   &pl))
         return false;
     a.kind = pl.kind; a.gy = pl.gy; a.gz = pl.gz; a.TRB = pl.TRB; a.nchunks = pl.nchunks;
     a.chunks_per_tile = pl.chunks_per_tile; a.rows_per_chunk = pl.rows_per_chunk;
@@ -187,6 +229,11 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
     a.F = pl.F; a.frag = pl.frag;
     if (a.kind == WGRAD_F32W) {
         a.lds_bytes = f32w_lds(a.C, a.R, a.S);
+    } else if (a.kind == WGRAD_KSLICE_BF16) {
+        // the staging buffers; after the loop the waves' sums (NW/2 of them at once)
+        const int bufs = KsliceGeom<kKsliceNW>::loop_lds;
+        const int red = kKsliceNW * ((4 * a.R * a.S + 1) / 2) * 1024;
+        a.lds_bytes = std::max(bufs, red);
     } else if (a.kind == WGRAD_STRIP_BF16 || a.kind == WGRAD_TAPS_BF16 || a.kind == WGRAD_TAPS2_BF16) {
         const int cb = a.kind == WGRAD_STRIP_BF16 ? 64 : 32;
         a.lds_bytes = ((a.TRB + 1) * cb * kXP + 2 * cb * kXP) * 2;
@@ -574,6 +621,288 @@ __global__ __launch_bounds__(kThreads) void wgrad_taps_bf16_kernel(WgradArgs a) 
         case 2: strip_body<SS, TRB, kTapSplit, 2>(a, smem); break;
         default: strip_body<SS, TRB, kTapSplit, 3>(a, smem); break;
     }
+}
+
+// ---------------------------------------------------------------- k-slice kernel (bf16)
+//
+// One 32 x 32 block (filters o0 .. o0+31, channels c0 .. c0+31) per workgroup
+// over a strip of 16 * NW output columns of one sample.  Wave w owns pixels
+// [16 w, 16 w + 16) of every output row (one MFMA k-step) and keeps all TR x SS
+// taps of the block in accumulators.  Per output row a wave reads from LDS
+// one dy fragment (A) and the fragment of the single x row that enters the
+// filter window (into the registers of the row that leaves it, once that
+// row's MFMAs have issued); the other TR - 1 x fragments stay in registers.
+// With four times fewer workgroups per output block than the 64 x 64 strip
+// kernel the partials are four times smaller.  At the end the waves' sums are
+// added in LDS in a fixed tree order (deterministic) and wave 0 stores the
+// partial in fragment order [chunk][block][tap][16][64].
+//
+// Staging copies rows global -> LDS with the 16-byte direct loads of gfx950
+// (lane l's 16 bytes land at the wave's LDS base + 16 l): no registers and no
+// VALU, so the rows of a step are requested kDepth steps ahead, one LDS
+// buffer per step in flight.  The plan admits only layers where every staged
+// element an MFMA reads lies inside the tile (channels and filters in whole
+// blocks of 32, whole strips, halo >= padding), so nothing is masked.  The
+// data of step j (x row j + TR - 1 of the window, dy row j) is requested in
+// step j - kDepth, waited for at the end of step j - 2 (each wave its own
+// loads, then the barrier), read into registers in step j - 1 and multiplied
+// in step j.
+
+// unit range [lo, hi) of range index k (r bits, first halving first) after r
+// halvings of [0, n): bit 0 keeps the lower half, bit 1 the upper
+__host__ __device__ constexpr int ks_lo(int n, int r, int k) {
+    int lo = 0, hi = n;
+    for (int b = r - 1; b >= 0; --b) {
+        const int mid = (lo + hi) / 2;
+        if ((k >> b) & 1) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+__host__ __device__ constexpr int ks_hi(int n, int r, int k) {
+    int lo = 0, hi = n;
+    for (int b = r - 1; b >= 0; --b) {
+        const int mid = (lo + hi) / 2;
+        if ((k >> b) & 1) lo = mid; else hi = mid;
+    }
+    return hi;
+}
+
+template <int TR, int SS, int NW, int DYSH>
+__global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a) {
+    using G = KsliceGeom<NW>;
+    constexpr int NT = TR * SS, P = G::P, XU8 = G::XU8, KD = G::kDepth;
+    constexpr int NSLOT = TR;                         // x fragments held in registers
+    constexpr int U = NSLOT % 2 == 0 ? NSLOT : 2 * NSLOT;
+    constexpr int UL = (U % KD == 0) ? U : (KD % U == 0 ? KD : U * KD);   // every index repeats
+    static_assert(SS <= 3 && TR <= 3, "a lane's x window is one 16-byte and one 4-byte read");
+    static_assert(DYSH == 0 || DYSH == 1, "dy window: at most one element past a 16-byte boundary");
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* const lds = reinterpret_cast<uint16_t*>(smem);
+
+    int c = blockIdx.x;
+    const int seg = c % a.nseg; c /= a.nseg;
+    const int qb = c % a.nqb; c /= a.nqb;
+    const int n = c % a.Nn;
+    const int tile = c / a.Nn;
+    const int p0 = seg * a.rows_per_seg;
+    const int nrows = min(a.rows_per_seg, a.Hot - p0);
+    const int q0 = qb * G::QW;
+    const int ncsb = a.C / 32;
+    const int o0 = (blockIdx.z / ncsb) * 32, c0 = (blockIdx.z % ncsb) * 32;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l32 = lane & 31, hi = lane >> 5;
+
+    const uint16_t* xt = static_cast<const uint16_t*>(a.x) + tile * a.x_tile +
+                         int64_t(n) * a.C * a.x_rows * a.x_pitch;
+    const int dy_rows = a.Hot + 2 * a.dy_off;
+    const uint16_t* dyt = static_cast<const uint16_t*>(a.dy) + tile * a.dy_tile +
+                          int64_t(n) * a.K * dy_rows * a.dy_pitch;
+    const int xg0 = q0 + a.base_c;                 // x column of staged column 0 (a multiple of 8)
+    const int dya0 = q0 + a.dy_off - DYSH;         // dy column of staged column 0 (a multiple of 8)
+    const int xrow0 = p0 + a.base_r;               // x row of window row 0 in step 0
+
+    // This wave's loads of a step: load k is number wave + k * NW of the
+    // step's 2 NI (x region, then dy region; past that: junk).  Lane offsets
+    // (bytes inside a sample, below 2^32 by the plan) are fixed; a step adds
+    // the row.
+    uint32_t loff[G::LPW];
+    int ldst[G::LPW];            // LDS element offset of the load's 64 chunks in a buffer
+    bool lx[G::LPW];             // the load reads x (else dy)
+    const uint32_t jx = uint32_t((int64_t(c0) * a.x_rows * a.x_pitch + xg0) * 2);   // a junk load's x chunk
+#pragma unroll
+    for (int k = 0; k < G::LPW; ++k) {
+        const int id = wave + k * NW;
+        const bool isx = id < G::NI || id >= 2 * G::NI;
+        const int ii = id < G::NI ? id : id - G::NI;
+        const int cc = min(64 * ii + lane, 32 * XU8 - 1);   // chunk (spare chunks repeat the last)
+        const int rr = cc / XU8, g8 = cc - rr * XU8;
+        if (id >= 2 * G::NI) {
+            loff[k] = jx;
+            ldst[k] = 2 * G::REG;
+        } else if (isx) {
+            loff[k] = uint32_t((int64_t(c0 + rr) * a.x_rows * a.x_pitch + min(xg0 + 8 * g8, a.x_pitch - 8)) * 2);
+            ldst[k] = 64 * ii * 8;
+        } else {
+            loff[k] = uint32_t((int64_t(o0 + rr) * dy_rows * a.dy_pitch + min(dya0 + 8 * g8, a.dy_pitch - 8)) * 2);
+            ldst[k] = G::REG + 64 * ii * 8;
+        }
+        lx[k] = isx;
+    }
+    // The loads are written out: the compiler would otherwise wait for every
+    // direct load before any LDS read.  The waits are wait_loads() below.
+    const uint32_t lds0 = static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) unsigned char*)smem));
+    auto dma = [](const char* base, uint32_t off, uint32_t ldsaddr) {
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                     :: "s"(ldsaddr), "v"(off), "s"(base) : "memory", "m0");
+    };
+    auto request = [&](int j, int b) {   // step j's rows -> LDS buffer b
+        const char* xr = reinterpret_cast<const char*>(
+            xt + int64_t(min(max(xrow0 + j + TR - 1, 0), a.x_rows - 1)) * a.x_pitch);
+        const char* dr = reinterpret_cast<const char*>(
+            dyt + int64_t(min(p0 + j + a.dy_off, dy_rows - 1)) * a.dy_pitch);
+#pragma unroll
+        for (int k = 0; k < G::LPW; ++k)
+            dma(lx[k] ? xr : dr, loff[k], lds0 + 2 * (b * G::BUF + ldst[k]));
+    };
+    auto request_x = [&](int m, int b) {   // window row m alone (its x loads; the rest repeat them)
+        const char* xr = reinterpret_cast<const char*>(
+            xt + int64_t(min(max(xrow0 + m, 0), a.x_rows - 1)) * a.x_pitch);
+#pragma unroll
+        for (int k = 0; k < G::LPW; ++k)
+            dma(xr, lx[k] ? loff[k] : jx, lds0 + 2 * (b * G::BUF + (lx[k] ? ldst[k] : 2 * G::REG)));
+    };
+    // wait for this wave's loads, all but the newest n steps
+    auto wait_loads = [](auto nc) {
+        constexpr int nl = decltype(nc)::value * G::LPW;
+        static_assert(nl < 64, "vmcnt range");
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(nl) : "memory");
+    };
+
+    // a lane's fragments: x channel c0 + l32 / dy filter o0 + l32, pixels 16 w + 8 hi .. + 7
+    const int fo = l32 * P + 16 * wave + 8 * hi;
+    uint32_t xf[NSLOT][5];     // 10 x elements: the window of shift s starts s elements in
+    uint4 A[2];
+    auto read_x = [&](const uint16_t* buf, auto slotc) {
+        constexpr int sl = decltype(slotc)::value;
+        const uint4 v = *reinterpret_cast<const uint4*>(buf + fo);
+        xf[sl][0] = v.x; xf[sl][1] = v.y; xf[sl][2] = v.z; xf[sl][3] = v.w;
+        xf[sl][4] = *reinterpret_cast<const uint32_t*>(buf + fo + 8);
+    };
+    auto read_dy = [&](const uint16_t* buf) {
+        const uint4 v = *reinterpret_cast<const uint4*>(buf + G::REG + fo);
+        if constexpr (DYSH == 0) return v;
+        const uint32_t e = *reinterpret_cast<const uint32_t*>(buf + G::REG + fo + 8);
+        return make_uint4(__builtin_amdgcn_alignbyte(v.y, v.x, 2), __builtin_amdgcn_alignbyte(v.z, v.y, 2),
+                          __builtin_amdgcn_alignbyte(v.w, v.z, 2), __builtin_amdgcn_alignbyte(e, v.w, 2));
+    };
+
+    floatx16 acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
+
+    // prologue, one round trip: window rows 0 .. TR-2 (buffers kDepth ..,
+    // into register slots 0 .. TR-2) and steps 0 .. kDepth-1 requested
+    // together; step 0 read into registers (slot TR-1, A[0])
+    static_for<0, TR - 1>([&](auto rc) { request_x(decltype(rc)::value, KD + decltype(rc)::value); });
+    static_for<0, KD>([&](auto jc) { request(decltype(jc)::value, decltype(jc)::value); });
+    wait_loads(std::integral_constant<int, KD - 1>{});
+    __syncthreads();
+    static_for<0, TR - 1>([&](auto rc) { read_x(lds + (KD + decltype(rc)::value) * G::BUF, rc); });
+    read_x(lds, std::integral_constant<int, TR - 1>{});
+    A[0] = read_dy(lds);
+    wait_loads(std::integral_constant<int, KD - 2>{});
+    __syncthreads();
+
+    // The MFMAs are written out (volatile): the LDS reads and the loads keep
+    // their place between them.  A B operand built by VALU (shifts, register
+    // copies) gets the two wait states an MFMA source needs after a VALU write.
+    auto step = [&](int i, auto Jc) __attribute__((always_inline)) {
+        constexpr int J = decltype(Jc)::value;
+        constexpr int SN = J % NSLOT;
+        const uint16_t* bn = lds + ((J + 1) % KD) * G::BUF;
+        request(i + KD, J % KD);              // into the buffer step i-1 read
+        A[(J + 1) % 2] = read_dy(bn);          // step i+1's dy fragment
+        Pack8 Av;
+        Av.v = A[J % 2];
+        static_for<0, NT>([&](auto tc) {
+            constexpr int t = decltype(tc)::value, r = t / SS, s = t % SS, sl = (J + r) % NSLOT;
+            Pack8 B;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                B.d[q] = s & 1 ? __builtin_amdgcn_alignbyte(xf[sl][q + s / 2 + 1], xf[sl][q + s / 2], 2)
+                               : xf[sl][q + s / 2];
+            if constexpr (s == 0)
+                asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc[t]) : "v"(Av.b), "v"(B.b));
+            else
+                asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                             : "+v"(acc[t]) : "v"(Av.b), "v"(B.b));
+            // step i+1's x row into the registers of window row 0, now issued
+            if constexpr (t == SS - 1) read_x(bn, std::integral_constant<int, SN>{});
+        });
+        wait_loads(std::integral_constant<int, KD - 2>{});   // step i+2's rows are in LDS
+        __syncthreads();
+    };
+    int i = 0;
+    for (; i + UL <= nrows; i += UL)
+        static_for<0, UL>([&](auto Jc) { step(i + decltype(Jc)::value, Jc); });
+    static_for<0, UL - 1>([&](auto Jc) {
+        if (i + decltype(Jc)::value < nrows) step(i + decltype(Jc)::value, Jc);
+    });
+    wait_loads(std::integral_constant<int, 0>{});   // no load may land in the LDS reused below
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < NT; ++t) asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(acc[t]));
+
+    // The waves' sums, by recursive halving: unit u = 4 t + q is the float4
+    // acc[t][4q .. 4q+3] of a lane.  In the round of distance D a wave and
+    // its partner wave ^ D hold the same unit range; the one without bit D
+    // keeps the lower half and hands over the upper, the other the reverse.
+    // After log2(NW) rounds wave w owns the sums of its own share of the
+    // units (in a fixed order of additions) and stores them.
+    constexpr int NU = 4 * NT, LOGW = NW == 8 ? 3 : NW == 4 ? 2 : 1;
+    static_assert(NW == (1 << LOGW), "power-of-two waves");
+    float4* red = reinterpret_cast<float4*>(smem);   // [wave][unit slot][64] float4
+    constexpr int SLOT = (NU + 1) / 2;               // units handed over in the first round
+    static_for<0, LOGW>([&](auto rc) {
+        constexpr int r = decltype(rc)::value, D = NW >> (r + 1);
+        const int path = wave >> (LOGW - r);          // the wave's range before this round
+        const bool upper = (wave & D) != 0;
+        float4* mine = red + wave * SLOT * 64 + lane;
+        const float4* theirs = red + (wave ^ D) * SLOT * 64 + lane;
+        static_for<0, (1 << r)>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            constexpr int LO = ks_lo(NU, r, k), HI = ks_hi(NU, r, k), MID = (LO + HI) / 2;
+            if (path == k) {
+                if (upper)
+                    static_for<LO, MID>([&](auto uc) {
+                        constexpr int u = decltype(uc)::value, q = u % 4;
+                        const floatx16& v = acc[u / 4];
+                        mine[(u - LO) * 64] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+                    });
+                else
+                    static_for<MID, HI>([&](auto uc) {
+                        constexpr int u = decltype(uc)::value, q = u % 4;
+                        const floatx16& v = acc[u / 4];
+                        mine[(u - MID) * 64] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+                    });
+            }
+        });
+        __syncthreads();
+        static_for<0, (1 << r)>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            constexpr int LO = ks_lo(NU, r, k), HI = ks_hi(NU, r, k), MID = (LO + HI) / 2;
+            auto add = [&](auto uc, int pos) {
+                constexpr int u = decltype(uc)::value, q = u % 4;
+                floatx16& v = acc[u / 4];
+                const float4 w = theirs[pos * 64];
+                v[4 * q] += w.x; v[4 * q + 1] += w.y; v[4 * q + 2] += w.z; v[4 * q + 3] += w.w;
+            };
+            if (path == k) {
+                if (upper)   // partner handed over [MID, HI) at slots 0 ..
+                    static_for<MID, HI>([&](auto uc) { add(uc, decltype(uc)::value - MID); });
+                else         // partner handed over [LO, MID)
+                    static_for<LO, MID>([&](auto uc) { add(uc, decltype(uc)::value - LO); });
+            }
+        });
+        __syncthreads();
+    });
+    // partial, [chunk][block][unit][64 lanes][4]: this wave's units
+    float4* part = reinterpret_cast<float4*>(a.part + int64_t(blockIdx.x) * a.F +
+                                             int64_t(blockIdx.z) * NT * 1024) + lane;
+    static_for<0, NW>([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        constexpr int LO = ks_lo(NU, LOGW, k), HI = ks_hi(NU, LOGW, k);
+        if (wave == k)
+            static_for<LO, HI>([&](auto uc) {
+                constexpr int u = decltype(uc)::value, q = u % 4;
+                const floatx16& v = acc[u / 4];
+                part[u * 64] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+            });
+    });
 }
 
 // ---------------------------------------------------------------- bf16
@@ -1049,6 +1378,21 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(WgradArgs a) {
         const int r = 2 * (tap / SP) + ((cp >> 1) & 1), s = 2 * (tap % SP) + (cp & 1);
         if (r >= a.R || s >= a.S || o >= a.K || ci >= a.C) return;
         idx = ((int64_t(o) * a.C + ci) * a.R + r) * a.S + s;
+    } else if (a.frag == 5) {
+        // [gz][tap][q][64 lanes][4]: value j of float4 q is fragment element e = 4 q + j
+        const int NT = a.R * a.S;
+        int64_t t = f;
+        const int j = int(t % 4); t /= 4;
+        const int lane = int(t % 64); t /= 64;
+        const int q = int(t % 4); t /= 4;
+        const int tap = int(t % NT); t /= NT;
+        const int bz = int(t);
+        const int ncsb = (a.C + 31) / 32;
+        const int o = (bz / ncsb) * 32 + 8 * q + 4 * (lane / 32) + j;
+        const int ci = (bz % ncsb) * 32 + (lane & 31);
+        const int r = tap / a.S, s = tap % a.S;
+        if (o >= a.K || ci >= a.C) return;
+        idx = ((int64_t(o) * a.C + ci) * a.R + r) * a.S + s;
     } else if (a.frag == 2) {
         // [gy][gz][tap][16][64] -> (o, ci, r, s), 32x32 blocks
         const int NT = a.TRB * a.S;
@@ -1118,6 +1462,15 @@ static hipError_t launch_f32wg(const WgradArgs& a, dim3 grid, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int TR, int SS, int DYSH>
+static hipError_t launch_kslice(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    auto k = wgrad_kslice_bf16_kernel<TR, SS, kKsliceNW, DYSH>;
+    hipError_t e = set_lds(k, a.lds_bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k, grid, dim3(64 * kKsliceNW), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
 template <int SS>
 static hipError_t launch_taps2(const WgradArgs& a, dim3 grid, hipStream_t s) {
     hipError_t e = set_lds(wgrad_taps2_bf16_kernel<SS, SS>, a.lds_bytes);
@@ -1163,6 +1516,11 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
         DC_F32WG(16, 3, 3)
         return hipErrorInvalidValue;
 #undef DC_F32WG
+    } else if (a.kind == WGRAD_KSLICE_BF16) {
+        // the dy columns of a strip start dy_off & 7 elements past a 16-byte boundary
+        if (a.R == 3 && a.S == 3 && (a.dy_off & 7) == 0) e = launch_kslice<3, 3, 0>(a, grid, s);
+        else if (a.R == 3 && a.S == 3 && (a.dy_off & 7) == 1) e = launch_kslice<3, 3, 1>(a, grid, s);
+        else return hipErrorInvalidValue;
     } else if (a.kind == WGRAD_TAPS2_BF16) {
         switch ((a.S + 1) / 2) {
             case 2: e = launch_taps2<2>(a, grid, s); break;

@@ -352,7 +352,7 @@ size_t dc_bwd_filter_workspace_bytes(const dc_problem* prob, int32_t tile) {
     if (make_geo_tile(prob, tile, &g) != DC_OK) return 0;
     int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
     return wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot,
-                                 g.h - g.pad);
+                                 g.h - g.pad, g.h);
 }
 
 dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x_pad,
@@ -366,7 +366,7 @@ dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x
     if (misaligned(x_pad) || misaligned(dy_pad) || misaligned(dw)) return DC_ERR_ALIGN;
     const int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
     size_t need = wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot,
-                                 g.h - g.pad);
+                                 g.h - g.pad, g.h);
     if (need > 0 && (!workspace || workspace_bytes < need)) return DC_ERR_WORKSPACE;
     if (need > 0 && misaligned(workspace)) return DC_ERR_ALIGN;
     WgradArgs a;

@@ -88,7 +88,7 @@ hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s);
 // summed over the chunk's (n, p, q).
 
 enum WgradKind { WGRAD_STRIP_BF16 = 0, WGRAD_ROWS_BF16 = 1, WGRAD_ROWS_F32 = 2, WGRAD_TAPS_BF16 = 3,
-                 WGRAD_TAPS2_BF16 = 4, WGRAD_F32W = 5 };
+                 WGRAD_TAPS2_BF16 = 4, WGRAD_F32W = 5, WGRAD_KSLICE_BF16 = 6 };
 
 struct WgradArgs {
     const void* x;               // padded x tiles
@@ -110,16 +110,17 @@ struct WgradArgs {
     int TRB;                     // filter rows per workgroup
     int nchunks;
     int chunks_per_tile, rows_per_chunk;   // row kinds: flattened (n, p) rows per chunk
-    int nqb, nseg, rows_per_seg;           // strip kind: 64-column strips, row segments
+    int nqb, nseg, rows_per_seg;           // strip kinds: column strips, row segments
     int64_t F;                   // floats per chunk partial
-    int frag;                    // 0: partials in dw order; 1 .. 4: in MFMA fragment order (64x64
+    int frag;                    // 0: partials in dw order; 1 .. 5: in MFMA fragment order (64x64
                                  // blocks, 32x32 blocks, 32x32 blocks of stride-2 phase images,
-                                 // fp32 32 filters x 32 flattened (ci, r, s))
+                                 // fp32 32 filters x 32 flattened (ci, r, s), 32x32 blocks as
+                                 // float4 per lane)
     int lds_bytes;
 };
 
 size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, int S,
-                             int stride, int Hot, int Wot, int base_c);
+                             int stride, int Hot, int Wot, int base_c, int dy_off);
 bool wgrad_plan(WgradArgs& a, int dtype);
 hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s);
 
