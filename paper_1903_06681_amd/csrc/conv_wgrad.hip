@@ -82,8 +82,9 @@ struct KsliceGeom {
     static constexpr int REG = NI * 64 * 8;       // elements of a block's region (spare chunks at the end)
     static constexpr int BUF = 2 * REG + 64 * 8;  // x region, dy region, 64 chunks nobody reads
     static constexpr int LPW = (2 * NI + NW - 1) / NW;   // loads per wave per step
-    static constexpr int kDepth = 4;              // steps between a row's request and its use
-    static constexpr int loop_lds = (kDepth + 2) * BUF * 2;   // + the first two window rows (3-row filters)
+    static constexpr int kDepth = 5;              // steps between a row's request and its use
+    static constexpr int nbuf = kDepth + 1;       // step buffers (a barrier every second step)
+    static constexpr int loop_lds = (nbuf + 2) * BUF * 2;   // + the first two window rows (3-row filters)
 };
 
 // k-slice kernel: instantiated filters, and whether a sample's x and dy
@@ -639,14 +640,15 @@ __global__ __launch_bounds__(kThreads) void wgrad_taps_bf16_kernel(WgradArgs a) 
 //
 // Staging copies rows global -> LDS with the 16-byte direct loads of gfx950
 // (lane l's 16 bytes land at the wave's LDS base + 16 l): no registers and no
-// VALU, so the rows of a step are requested kDepth steps ahead, one LDS
-// buffer per step in flight.  The plan admits only layers where every staged
-// element an MFMA reads lies inside the tile (channels and filters in whole
-// blocks of 32, whole strips, halo >= padding), so nothing is masked.  The
-// data of step j (x row j + TR - 1 of the window, dy row j) is requested in
-// step j - kDepth, waited for at the end of step j - 2 (each wave its own
-// loads, then the barrier), read into registers in step j - 1 and multiplied
-// in step j.
+// VALU, so the rows of a step are requested kDepth steps ahead.  The plan
+// admits only layers where every staged element an MFMA reads lies inside
+// the tile (channels and filters in whole blocks of 32, whole strips, halo >=
+// padding), so nothing is masked.  The data of step j (x row j + TR - 1 of the
+// window, dy row j) goes to buffer j % nbuf: requested in step j - kDepth,
+// read into registers in step j - 1, multiplied in step j.  A barrier ends
+// every odd step, after each wave has waited for its loads of the next two
+// steps' data; with nbuf = kDepth + 1 a buffer is requested again only after
+// a barrier has passed its last read.
 
 // unit range [lo, hi) of range index k (r bits, first halving first) after r
 // halvings of [0, n): bit 0 keeps the lower half, bit 1 the upper
@@ -670,10 +672,11 @@ __host__ __device__ constexpr int ks_hi(int n, int r, int k) {
 template <int TR, int SS, int NW, int DYSH>
 __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a) {
     using G = KsliceGeom<NW>;
-    constexpr int NT = TR * SS, P = G::P, XU8 = G::XU8, KD = G::kDepth;
+    constexpr int NT = TR * SS, P = G::P, XU8 = G::XU8, KD = G::kDepth, NB = G::nbuf;
     constexpr int NSLOT = TR;                         // x fragments held in registers
     constexpr int U = NSLOT % 2 == 0 ? NSLOT : 2 * NSLOT;
-    constexpr int UL = (U % KD == 0) ? U : (KD % U == 0 ? KD : U * KD);   // every index repeats
+    constexpr int UL = (U % NB == 0) ? U : (NB % U == 0 ? NB : U * NB);   // every index repeats
+    static_assert(UL % 2 == 0 && KD >= 3, "barrier parity, two steps of data ahead");
     static_assert(SS <= 3 && TR <= 3, "a lane's x window is one 16-byte and one 4-byte read");
     static_assert(DYSH == 0 || DYSH == 1, "dy window: at most one element past a 16-byte boundary");
     extern __shared__ __align__(16) unsigned char smem[];
@@ -784,17 +787,18 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
 
-    // prologue, one round trip: window rows 0 .. TR-2 (buffers kDepth ..,
+    // prologue, one round trip: window rows 0 .. TR-2 (buffers nbuf ..,
     // into register slots 0 .. TR-2) and steps 0 .. kDepth-1 requested
-    // together; step 0 read into registers (slot TR-1, A[0])
-    static_for<0, TR - 1>([&](auto rc) { request_x(decltype(rc)::value, KD + decltype(rc)::value); });
+    // together; step 0 read into registers (slot TR-1, A[0]); steps 1 and 2
+    // in LDS before the loop (as after an odd step)
+    static_for<0, TR - 1>([&](auto rc) { request_x(decltype(rc)::value, NB + decltype(rc)::value); });
     static_for<0, KD>([&](auto jc) { request(decltype(jc)::value, decltype(jc)::value); });
     wait_loads(std::integral_constant<int, KD - 1>{});
     __syncthreads();
-    static_for<0, TR - 1>([&](auto rc) { read_x(lds + (KD + decltype(rc)::value) * G::BUF, rc); });
+    static_for<0, TR - 1>([&](auto rc) { read_x(lds + (NB + decltype(rc)::value) * G::BUF, rc); });
     read_x(lds, std::integral_constant<int, TR - 1>{});
     A[0] = read_dy(lds);
-    wait_loads(std::integral_constant<int, KD - 2>{});
+    wait_loads(std::integral_constant<int, KD - 3>{});
     __syncthreads();
 
     // The MFMAs are written out (volatile): the LDS reads and the loads keep
@@ -803,8 +807,8 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
     auto step = [&](int i, auto Jc) __attribute__((always_inline)) {
         constexpr int J = decltype(Jc)::value;
         constexpr int SN = J % NSLOT;
-        const uint16_t* bn = lds + ((J + 1) % KD) * G::BUF;
-        request(i + KD, J % KD);              // into the buffer step i-1 read
+        const uint16_t* bn = lds + ((J + 1) % NB) * G::BUF;
+        request(i + KD, (J + KD) % NB);       // last read in step i-2, a barrier ago
         A[(J + 1) % 2] = read_dy(bn);          // step i+1's dy fragment
         Pack8 Av;
         Av.v = A[J % 2];
@@ -823,8 +827,10 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
             // step i+1's x row into the registers of window row 0, now issued
             if constexpr (t == SS - 1) read_x(bn, std::integral_constant<int, SN>{});
         });
-        wait_loads(std::integral_constant<int, KD - 2>{});   // step i+2's rows are in LDS
-        __syncthreads();
+        if constexpr (J % 2 == 1) {
+            wait_loads(std::integral_constant<int, KD - 3>{});   // steps i+2 and i+3 are in LDS
+            __syncthreads();
+        }
     };
     int i = 0;
     for (; i + UL <= nrows; i += UL)
