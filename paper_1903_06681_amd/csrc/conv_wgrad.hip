@@ -80,7 +80,7 @@ struct KsliceGeom {
     static constexpr int P = 8 * XU8;             // staged row pitch (elements): rows 4 banks apart
     static constexpr int NI = (32 * XU8 + 63) / 64;   // 64-chunk loads per staged block (x or dy)
     static constexpr int REG = NI * 64 * 8;       // elements of a block's region (spare chunks at the end)
-    static constexpr int BUF = 2 * REG + 64 * 8;  // x region, dy region, 64 chunks nobody reads
+    static constexpr int BUF = 2 * REG + 64 * 8;  // x region, dy region, 64 chunks nobody reads (prologue)
     static constexpr int LPW = (2 * NI + NW - 1) / NW;   // loads per wave per step
     static constexpr int kDepth = 5;              // steps between a row's request and its use
     static constexpr int nbuf = kDepth + 1;       // step buffers (a barrier every second step)
@@ -706,13 +706,15 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
     const int xrow0 = p0 + a.base_r;               // x row of window row 0 in step 0
 
     // This wave's loads of a step: load k is number wave + k * NW of the
-    // step's 2 NI (x region, then dy region; past that: junk).  Lane offsets
-    // (bytes inside a sample, below 2^32 by the plan) are fixed; a step adds
-    // the row.
+    // step's 2 NI (x region, then dy region); only waves below NX have a load
+    // in the last slot.  Lane offsets (bytes inside a sample, below 2^32 by
+    // the plan) are fixed; a step adds the row.
     uint32_t loff[G::LPW];
     int ldst[G::LPW];            // LDS element offset of the load's 64 chunks in a buffer
     bool lx[G::LPW];             // the load reads x (else dy)
     const uint32_t jx = uint32_t((int64_t(c0) * a.x_rows * a.x_pitch + xg0) * 2);   // a junk load's x chunk
+    constexpr int NX = 2 * G::NI - (G::LPW - 1) * NW;   // waves with LPW loads a step (the rest LPW - 1)
+    const bool full = wave < NX;
 #pragma unroll
     for (int k = 0; k < G::LPW; ++k) {
         const int id = wave + k * NW;
@@ -747,20 +749,25 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
             dyt + int64_t(min(p0 + j + a.dy_off, dy_rows - 1)) * a.dy_pitch);
 #pragma unroll
         for (int k = 0; k < G::LPW; ++k)
-            dma(lx[k] ? xr : dr, loff[k], lds0 + 2 * (b * G::BUF + ldst[k]));
+            if (k < G::LPW - 1 || full) dma(lx[k] ? xr : dr, loff[k], lds0 + 2 * (b * G::BUF + ldst[k]));
     };
     auto request_x = [&](int m, int b) {   // window row m alone (its x loads; the rest repeat them)
         const char* xr = reinterpret_cast<const char*>(
             xt + int64_t(min(max(xrow0 + m, 0), a.x_rows - 1)) * a.x_pitch);
 #pragma unroll
         for (int k = 0; k < G::LPW; ++k)
-            dma(xr, lx[k] ? loff[k] : jx, lds0 + 2 * (b * G::BUF + (lx[k] ? ldst[k] : 2 * G::REG)));
+            if (k < G::LPW - 1 || full)
+                dma(xr, lx[k] ? loff[k] : jx, lds0 + 2 * (b * G::BUF + (lx[k] ? ldst[k] : 2 * G::REG)));
     };
-    // wait for this wave's loads, all but the newest n steps
-    auto wait_loads = [](auto nc) {
-        constexpr int nl = decltype(nc)::value * G::LPW;
-        static_assert(nl < 64, "vmcnt range");
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(nl) : "memory");
+    // wait for this wave's loads, all but the newest n steps' (the count of
+    // a step depends on the wave; the branch is uniform)
+    auto wait_loads = [&](auto nc) {
+        constexpr int n = decltype(nc)::value;
+        static_assert(n * G::LPW < 64, "vmcnt range");
+        if (full)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n * G::LPW) : "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n * (G::LPW - 1)) : "memory");
     };
 
     // a lane's fragments: x channel c0 + l32 / dy filter o0 + l32, pixels 16 w + 8 hi .. + 7
