@@ -96,6 +96,11 @@ SMALL = {
     # stride 2 with at most 4 channels: the forward pass on the phase images
     "s2ph5_bf16": Layer("s2ph5_bf16", 2, 4, 48, 36, 52, 5, 5, 2, 2, 2, 2, 2, "bf16", "uniform", 95),
     "s2ph3_bf16": Layer("s2ph3_bf16", 2, 2, 24, 32, 32, 3, 3, 2, 1, 2, 2, 1, "bf16", "uniform", 96),
+    # 3x3 on whole 32-blocks and 128-column tiles: the k-slice weight
+    # gradient (two-row segments: only the guarded tail steps; and one row
+    # per segment with 16-byte-aligned dy rows: halo 8, no padding)
+    "kslice_bf16": Layer("kslice_bf16", 1, 32, 32, 256, 256, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 97),
+    "kslice_p0_bf16": Layer("kslice_p0_bf16", 1, 32, 32, 130, 130, 3, 3, 1, 0, 1, 1, 8, "bf16", "uniform", 98),
 }
 
 
@@ -145,7 +150,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
                                   "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16",
-                                  "s2ph5_bf16"])
+                                  "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
