@@ -291,6 +291,8 @@ static int lds_bytes_for(const IgemmArgs& a, int dtype, int CC, int OB) {
 
 bool igemm_plan(IgemmArgs& a, int dtype) {
     a.kind = 0;
+    // a merged-phase backward-data request runs on the register-weight kernel or not at all
+    if (a.bp) return dtype == 1 && igemm_wreg_plan(a);
     if (dtype == 1 && igemm_wreg_plan(a)) return true;
     if (dtype == 0 && igemm_f32w_plan(a)) return true;
     a.OB = a.Cout <= 32 ? 32 : 64;

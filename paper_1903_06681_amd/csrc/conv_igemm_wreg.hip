@@ -46,8 +46,18 @@ __device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[
 // phase filter.  Ring row m holds phase row u0 + m: each staging block loads
 // the two 16-byte chunks of four (ci, pr) rows and keeps the columns of one
 // parity per phase channel.
-template <int NOB, int TR, int TS, int CG, int MINWG, bool PH = false>
+//
+// BP (MODE 2; backward-data at stride 2 with at most 8 channels): the four
+// output phases of Eq. (3) as one stride-1 correlation over dy.  Row o' =
+// 4 c + 2 py + px of the weight image is output channel c at phase (py, px);
+// window tap (a, b) holds filter tap (r0[py] - 2 (a - dr[py]), s0[px] - 2 (b -
+// dc[px])), zero outside phase (py, px)'s own taps.  Output pixel (u, v) of
+// the phase grid goes to dx[c][2u + py][2v + px].  The strips start bpvoff
+// pixels early so that the staged dy columns are 16-byte aligned; pixels
+// v < 0 are not stored.
+template <int NOB, int TR, int TS, int CG, int MINWG, int MODE = 0>
 __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs a) {
+    constexpr bool PH = MODE == 1, BP = MODE == 2;
     constexpr int KS = TR * TS * CG;          // 16-wide k-steps: (tap, 16-channel group)
     constexpr int CIN = CG * 16;
     constexpr int PS = 8 * ((CIN / 8) | 1);   // ring pixel stride (elements)
@@ -73,7 +83,7 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     const int tile = c / a.Nn;
     const int u0 = seg * a.rows_per_seg;
     const int u_end = min(u0 + a.rows_per_seg, a.Uo);
-    const int v0 = vb * 64;
+    const int v0 = vb * 64 - (BP ? a.bpvoff : 0);
     const int o0 = blockIdx.y * OBT;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int l32 = lane & 31, hi = lane >> 5;
@@ -182,7 +192,17 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     uint16_t* Wl = lds;
     {
         const uint16_t* w = static_cast<const uint16_t*>(a.w);
-        if constexpr (PH) {
+        if constexpr (BP) {
+            // merged-phase image: Wl[o'][k][a * TS + b] (o' = 4 c + 2 py + px, k = dy channel)
+            for (int e = tid; e < OBT * RL; e += kWThreads) {
+                const int o = e / RL, r_ = e % RL, ci = r_ / T, t = r_ % T;
+                const int c = o >> 2, py = (o >> 1) & 1, px = o & 1;
+                const int tr = t / TS - a.bpdr[py], ts = t % TS - a.bpdc[px];
+                const bool ok = c < a.bpC && tr >= 0 && tr < a.bptr[py] && ts >= 0 && ts < a.bpts[px];
+                const int r = a.bpr0[py] - 2 * tr, sx = a.bps0[px] - 2 * ts;
+                Wl[o * PW + r_] = ok ? w[((int64_t(ci) * a.wC + c) * a.R + r) * a.S + sx] : uint16_t(0);
+            }
+        } else if constexpr (PH) {
             // phase weights: Wl[o][c'][t'] = w[o0+o][ci][2r'+pr][2s'+pc], zero past
             // the filter and for the padding channels
             for (int e = tid; e < OBT * RL; e += kWThreads) {
@@ -327,10 +347,24 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     float* const out = a.out + tile * a.out_tile + (int64_t(n) * a.Cout + o0 + 4 * hi) * oplane +
                        int64_t(v) * a.ostr + a.oph_c;
     // every lane's pixel and every channel of the block in range: stores need no masks
-    const bool block_full = (v0 + 64 <= a.Vo) && (o0 + OBT <= a.Cout);
+    const bool block_full = !BP && (v0 + 64 <= a.Vo) && (o0 + OBT <= a.Cout);
     auto out_row = [&](int u) { return out + int64_t(u * a.ostr + a.oph_r) * a.out_cols; };
     // D layout: value e of lane l is output channel 8*(e/4) + 4*(l/32) + e%4, pixel l%32
     auto store_masked = [&](const floatx16 (&acc)[NOB], int u) {
+        if constexpr (BP) {
+            // row o' = 8 (e/4) + 4 hi + e%4 = 4 c + 2 py + px: c = 2 (e/4) + hi
+            if (u < u_end && v >= 0 && v < a.Vo) {
+                const int64_t plane = int64_t(a.out_rows) * a.out_cols;
+                float* const o = a.out + tile * a.out_tile + (int64_t(n) * a.bpC + hi) * plane +
+                                 int64_t(2 * u) * a.out_cols + 2 * v;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int c = 2 * (e / 4) + hi, py = (e % 4) / 2, px = e % 2;
+                    if (c < a.bpC) o[int64_t(2 * (e / 4)) * plane + py * a.out_cols + px] = acc[0][e];
+                }
+            }
+            return;
+        }
         if (u < u_end && v < a.Vo) {
             float* orow = out_row(u);
 #pragma unroll
@@ -457,7 +491,30 @@ static void wreg_segments(IgemmArgs& a) {
     a.nseg = (a.Uo + rps - 1) / rps;
 }
 
+// merged-phase backward-data: instantiated (window, 16-channel groups) shapes
+static bool wreg_bp_shape(int TR, int TS, int CG) {
+    return (TR == 4 && TS == 4 && CG == 4) || (TR == 2 && TS == 2 && CG == 4);
+}
+
 bool igemm_wreg_plan(IgemmArgs& a) {
+    if (a.bp) {
+        // the caller's merged-phase request (see the kernel's BP mode)
+        a.phase = 0;
+        if (a.Cout > 32 || a.Cin % 16 != 0 || !wreg_bp_shape(a.Tr, a.Ts, a.Cin / 16)) return false;
+        if (a.in_pitch % 8 != 0) return false;
+        a.bpvoff = a.base_c % 8;                   // strips start this many pixels early
+        const int lds = wreg_lds(1, a.Tr, a.Ts, a.Cin / 16);
+        if (lds > device_lds_limit()) return false;
+        a.OB = 32;
+        a.wvec = 0;
+        const int vo = a.Vo;
+        a.Vo = vo + a.bpvoff;                      // the strips cover the early pixels too
+        wreg_segments(a);
+        a.Vo = vo;
+        a.lds_bytes = lds;
+        a.kind = 1;
+        return true;
+    }
     a.phase = 0;
     if (a.wmode == 0 && a.istr == 2 && a.ostr == 1 && 4 * a.Cin <= 16 && a.base_c % 8 == 0 &&
         a.in_pitch % 8 == 0 && a.Tr == a.R && a.Ts == a.S) {
@@ -498,9 +555,9 @@ bool igemm_wreg_plan(IgemmArgs& a) {
     return true;
 }
 
-template <int NOB, int TR, int TS, int CG, int MINWG, bool PH = false>
+template <int NOB, int TR, int TS, int CG, int MINWG, int MODE = 0>
 static hipError_t launch_one(const IgemmArgs& a, hipStream_t s) {
-    auto k = igemm_wreg_kernel<NOB, TR, TS, CG, MINWG, PH>;
+    auto k = igemm_wreg_kernel<NOB, TR, TS, CG, MINWG, MODE>;
     if (a.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
@@ -513,9 +570,14 @@ static hipError_t launch_one(const IgemmArgs& a, hipStream_t s) {
 
 hipError_t launch_igemm_wreg(const IgemmArgs& a, hipStream_t s) {
     const int NOB = a.OB / 32, CG = a.Cin / 16;
+    if (a.bp) {
+        if (a.Tr == 4 && a.Ts == 4 && CG == 4) return launch_one<1, 4, 4, 4, 1, 2>(a, s);
+        if (a.Tr == 2 && a.Ts == 2 && CG == 4) return launch_one<1, 2, 2, 4, 1, 2>(a, s);
+        return hipErrorInvalidValue;
+    }
     if (a.phase) {
 #define DC_WREG_PH(nob, t) \
-        if (NOB == nob && a.Tr == t && a.Ts == t) return launch_one<nob, t, t, 1, 1, true>(a, s);
+        if (NOB == nob && a.Tr == t && a.Ts == t) return launch_one<nob, t, t, 1, 1, 1>(a, s);
         DC_WREG_PH(2, 4) DC_WREG_PH(1, 4) DC_WREG_PH(2, 2) DC_WREG_PH(1, 2) DC_WREG_PH(2, 3) DC_WREG_PH(1, 3)
 #undef DC_WREG_PH
         return hipErrorInvalidValue;

@@ -303,6 +303,50 @@ dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_
     if (misaligned(dy_pad) || misaligned(w) || misaligned(dx)) return DC_ERR_ALIGN;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int st_ = g.stride;
+    // Stride 2 with at most 8 channels: the four output phases below share
+    // one stride-1 correlation over dy, whose window is the union of theirs;
+    // one launch computes all of them (4 C rows of the MFMA block instead of
+    // C per launch).
+    if (st_ == 2 && g.dtype == DC_BF16 && 4 * g.C <= 32 && g.Ht % 2 == 0 && g.Wt % 2 == 0) {
+        IgemmArgs a;
+        igemm_common(g, tile, a);
+        a.in = dy_pad; a.w = w; a.out = dx;
+        a.in_tile = g.dy_tile;
+        a.out_tile = int64_t(g.N) * g.C * g.Ht * g.Wt;
+        a.Cin = g.K; a.Cout = 4 * g.C;
+        a.in_rows = g.dy_rows; a.in_cols = g.dy_cols; a.in_pitch = g.dy_pitch;
+        a.out_rows = g.Ht; a.out_cols = g.Wt;
+        a.ostr = 2; a.istr = 1;
+        a.Uo = g.Ht / 2; a.Vo = g.Wt / 2;
+        int br[2], bc[2];
+        bool ok = true;
+        for (int ph = 0; ph < 2; ++ph) {
+            const int rr = (ph + g.pad) % 2, rc = (ph + g.pad) % 2;
+            const int tr = rr < g.R ? (g.R - rr + 1) / 2 : 0, ts = rc < g.S ? (g.S - rc + 1) / 2 : 0;
+            if (tr == 0 || ts == 0) ok = false;
+            a.bptr[ph] = tr; a.bpts[ph] = ts;
+            br[ph] = g.h + (ph + g.pad - rr) / 2 - (tr - 1);
+            bc[ph] = g.h + (ph + g.pad - rc) / 2 - (ts - 1);
+            a.bpr0[ph] = rr + 2 * (tr - 1);
+            a.bps0[ph] = rc + 2 * (ts - 1);
+        }
+        a.base_r = std::min(br[0], br[1]);
+        a.base_c = std::min(bc[0], bc[1]);
+        a.Tr = a.Ts = 0;
+        for (int ph = 0; ph < 2; ++ph) {
+            a.bpdr[ph] = br[ph] - a.base_r;
+            a.bpdc[ph] = bc[ph] - a.base_c;
+            a.Tr = std::max(a.Tr, a.bpdr[ph] + a.bptr[ph]);
+            a.Ts = std::max(a.Ts, a.bpdc[ph] + a.bpts[ph]);
+        }
+        a.bp = 1; a.bpC = g.C;
+        a.w_os = int64_t(g.R) * g.S; a.w_cs = int64_t(g.C) * g.R * g.S;
+        a.wmode = 0;
+        if (ok && a.base_r >= 0 && a.base_c >= 0 && igemm_plan(a, g.dtype)) {
+            clear_stale_error();
+            return launched(launch_igemm(a, g.dtype, s));
+        }
+    }
     // Eq. (3) split by output phase (i mod stride, j mod stride): each phase
     // is a stride-1 correlation of dy with the taps r = (phase+pad) mod stride
     // + stride*t, visited in reverse.  At stride 1 there is one phase holding

@@ -65,6 +65,14 @@ struct IgemmArgs {
     int lds_bytes;
     int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32)
     int phase;                   // register-weight bf16 forward over the stride-2 phase images
+    // merged-phase backward-data (stride 2, C <= 8): all four output phases
+    // as one stride-1 correlation over dy; rows o' = 4 c + 2 py + px of the
+    // weight image, window origin (base_r, base_c).  bp: requested by the
+    // caller; bpC: C; bpvoff: pixels the strips start early (16-byte aligned
+    // staging); per row phase py: window-row offset bpdr, taps bptr, first
+    // filter row bpr0 (then -2 per window row); per column phase likewise
+    int bp, bpC, bpvoff;
+    int bpdr[2], bptr[2], bpr0[2], bpdc[2], bpts[2], bps0[2];
     int nvb, nseg, rows_per_seg; // strip kernel: 64-column strips, row segments
 };
 

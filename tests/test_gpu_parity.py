@@ -101,6 +101,11 @@ SMALL = {
     # per segment with 16-byte-aligned dy rows: halo 8, no padding)
     "kslice_bf16": Layer("kslice_bf16", 1, 32, 32, 256, 256, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 97),
     "kslice_p0_bf16": Layer("kslice_p0_bf16", 1, 32, 32, 130, 130, 3, 3, 1, 0, 1, 1, 8, "bf16", "uniform", 98),
+    # stride 2 with at most 8 channels and 64 filters: the input gradient's
+    # four output phases in one launch (7x7 window 4x4, 3x3 window 2x2;
+    # decomposed, window origins not 16-byte aligned)
+    "bp7_bf16": Layer("bp7_bf16", 2, 3, 64, 64, 64, 7, 7, 2, 3, 2, 2, 3, "bf16", "uniform", 99),
+    "bp3_bf16": Layer("bp3_bf16", 2, 8, 64, 48, 48, 3, 3, 2, 1, 2, 2, 1, "bf16", "uniform", 100),
 }
 
 
@@ -150,7 +155,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
                                   "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16",
-                                  "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16"])
+                                  "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16", "bp7_bf16", "bp3_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
