@@ -55,7 +55,11 @@ __device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[
 // the phase grid goes to dx[c][2u + py][2v + px].  The strips start bpvoff
 // pixels early so that the staged dy columns are 16-byte aligned; pixels
 // v < 0 are not stored.
-template <int NOB, int TR, int TS, int CG, int MINWG, int MODE = 0>
+// MF: the tile's pixel count is not a multiple of 64, so some strips are
+// partial; their stores stay inside the MFMA stream, masked per lane (a
+// separate instantiation, so that layers with whole strips keep exactly the
+// code they had: that kernel is sensitive to small changes in its schedule).
+template <int NOB, int TR, int TS, int CG, int MINWG, int MODE = 0, bool MF = false>
 __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs a) {
     constexpr bool PH = MODE == 1, BP = MODE == 2;
     constexpr int KS = TR * TS * CG;          // 16-wide k-steps: (tap, 16-channel group)
@@ -347,7 +351,7 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     float* const out = a.out + tile * a.out_tile + (int64_t(n) * a.Cout + o0 + 4 * hi) * oplane +
                        int64_t(v) * a.ostr + a.oph_c;
     // every lane's pixel and every channel of the block in range: stores need no masks
-    const bool block_full = !BP && (v0 + 64 <= a.Vo) && (o0 + OBT <= a.Cout);
+    const bool block_full = !BP && (MF || v0 + 64 <= a.Vo) && (o0 + OBT <= a.Cout);
     auto out_row = [&](int u) { return out + int64_t(u * a.ostr + a.oph_r) * a.out_cols; };
     // D layout: value e of lane l is output channel 8*(e/4) + 4*(l/32) + e%4, pixel l%32
     auto store_masked = [&](const floatx16 (&acc)[NOB], int u) {
@@ -406,7 +410,11 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
         auto store_prev = [&](auto sc) {
             constexpr int s = decltype(sc)::value, sob = s / 16, e = s % 16;
             constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
-            __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+            if constexpr (MF) {
+                if (v < a.Vo) __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+            } else {
+                __builtin_nontemporal_store(prev[sob][e], prow + int64_t(oc) * oplane);
+            }
         };
         auto mfmas = [&](auto with_stores) {
             // B operands run kPre k-steps ahead of the MFMAs that consume them
@@ -557,6 +565,19 @@ bool igemm_wreg_plan(IgemmArgs& a) {
 
 template <int NOB, int TR, int TS, int CG, int MINWG, int MODE = 0>
 static hipError_t launch_one(const IgemmArgs& a, hipStream_t s) {
+    if constexpr (MODE != 2) {   // partial strips: the masked-store instantiation
+        if (a.Vo % 64 != 0) {
+            auto k = igemm_wreg_kernel<NOB, TR, TS, CG, MINWG, MODE, true>;
+            if (a.lds_bytes > 64 * 1024) {
+                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
+                if (e != hipSuccess) return e;
+            }
+            dim3 grid(a.ntiles * a.Nn * a.nvb * a.nseg, (a.Cout + a.OB - 1) / a.OB);
+            hipLaunchKernelGGL(k, grid, dim3(kWThreads), a.lds_bytes, s, a);
+            return hipGetLastError();
+        }
+    }
     auto k = igemm_wreg_kernel<NOB, TR, TS, CG, MINWG, MODE>;
     if (a.lds_bytes > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k),
