@@ -293,6 +293,7 @@ bool igemm_plan(IgemmArgs& a, int dtype) {
     a.kind = 0;
     // a merged-phase backward-data request runs on the register-weight kernel or not at all
     if (a.bp) return dtype == 1 && igemm_wreg_plan(a);
+    if (dtype == 1 && igemm_roll_plan(a)) return true;
     if (dtype == 1 && igemm_wreg_plan(a)) return true;
     if (dtype == 0 && igemm_f32w_plan(a)) return true;
     a.OB = a.Cout <= 32 ? 32 : 64;
@@ -323,6 +324,7 @@ bool igemm_plan(IgemmArgs& a, int dtype) {
 hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
     if (a.kind == 1) return launch_igemm_wreg(a, s);
     if (a.kind == 2) return launch_igemm_f32w(a, s);
+    if (a.kind == 3) return launch_igemm_roll(a, s);
     const int nvb = (a.Vo + kBW - 1) / kBW, nub = (a.Uo + kBH - 1) / kBH;
     dim3 grid(nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
     dim3 block(kThreads);

@@ -63,7 +63,8 @@ struct IgemmArgs {
     int CC;                      // channels per LDS chunk (multiple of 8 for bf16, 2 for fp32)
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
-    int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32)
+    int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32);
+                                 // 3: register-weight rolling-row kernel (bf16)
     int phase;                   // register-weight bf16 forward over the stride-2 phase images
     // merged-phase backward-data (stride 2, C <= 8): all four output phases
     // as one stride-1 correlation over dy; rows o' = 4 c + 2 py + px of the
@@ -73,7 +74,7 @@ struct IgemmArgs {
     // filter row bpr0 (then -2 per window row); per column phase likewise
     int bp, bpC, bpvoff;
     int bpdr[2], bptr[2], bpr0[2], bpdc[2], bpts[2], bps0[2];
-    int nvb, nseg, rows_per_seg; // strip kernel: 64-column strips, row segments
+    int nvb, nseg, rows_per_seg; // strip kernels: 64- (128-, rolling) column strips, row segments
 };
 
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
@@ -84,6 +85,8 @@ bool igemm_plan(IgemmArgs& a, int dtype);
 hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s);
 bool igemm_wreg_plan(IgemmArgs& a);
 hipError_t launch_igemm_wreg(const IgemmArgs& a, hipStream_t s);
+bool igemm_roll_plan(IgemmArgs& a);
+hipError_t launch_igemm_roll(const IgemmArgs& a, hipStream_t s);
 bool igemm_f32w_plan(IgemmArgs& a);
 hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s);
 
