@@ -290,11 +290,18 @@ __global__ __launch_bounds__(kRThreads, 1) void igemm_roll_kernel(IgemmArgs a) {
     auto store_set = [&](auto setc, auto sc, int q) __attribute__((always_inline)) {   // store s of output row q
         constexpr int SET = decltype(setc)::value, s = decltype(sc)::value, sob = s / 16, e = s % 16;
         constexpr int oc = sob * 32 + 8 * (e / 4) + e % 4;
-        // (the element goes through a scalar first: a bit cast of a vector
-        // element lvalue reads element 0 with this compiler)
+        // Stored straight from the accumulator register: the builtin store
+        // copies every value to a VGPR first, and with the VGPRs full those
+        // copies share registers with the staged input rows.  The set's last
+        // MFMA ended a step earlier (drained), and phase B overwrites the set
+        // only 2 NOB MFMAs after the last store.  Nothing in the kernel reads
+        // the output, so no memory clobber and no wait on the store.
+        // (operands through locals: this compiler does not capture variables
+        // that a lambda names only in asm operands)
         const float f = acc[SET][sob][e];
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, f), rout, voff_out,
-                                              (u0 + q) * ocol4 + oc * opl4, 2 /* non-temporal */);
+        const int vo = voff_out, so = (u0 + q) * ocol4 + oc * opl4;
+        const __amdgpu_buffer_rsrc_t rs = rout;
+        asm volatile("buffer_store_dword %0, %1, %2, %3 offen nt" : : "a"(f), "v"(vo), "s"(rs), "s"(so));
     };
 
     // One step: input row j, register set J = j mod TR, filter rows
