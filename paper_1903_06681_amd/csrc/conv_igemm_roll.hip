@@ -140,22 +140,38 @@ __global__ __launch_bounds__(kRThreads, 1) void igemm_roll_kernel(IgemmArgs a) {
     // tile only feed pixels that are not stored
     const int gcol = min(a.base_c + v0 + pg * 8, a.in_pitch - 8);
     const int voff_in = int((int64_t(cg8 * 8) * plane + gcol) * 2);
-    uint4 stg[8];
+    // The row loads and the output stores are written as instructions the
+    // compiler does not see, so that its waits on the vector-memory counter
+    // do not cover the stores: store_row waits for the loads itself, leaving
+    // the NV stores issued since the loads in flight (the counter completes
+    // in issue order).
+    roll_v4u stg[8];
     auto load_row = [&](int m) __attribute__((always_inline)) {                // input row m of the segment -> registers
         if (stager) {
             const int gr = min(max(xr0 + m, 0), a.in_rows - 1);
             const int so = gr * a.in_pitch * 2;
+            const int vo = voff_in;
+            const __amdgpu_buffer_rsrc_t rs = rin;
 #pragma unroll
             for (int jj = 0; jj < 8; ++jj) {
-                const roll_v4u v = __builtin_amdgcn_raw_buffer_load_b128(rin, voff_in, so + int(jj * plane * 2), 0);
-                stg[jj] = make_uint4(v.x, v.y, v.z, v.w);
+                const int sj = so + int(jj * plane * 2);
+                asm volatile("buffer_load_dwordx4 %0, %1, %2, %3 offen" : "=v"(stg[jj]) : "v"(vo), "s"(rs), "s"(sj));
             }
         }
     };
-    auto store_row = [&](int m) __attribute__((always_inline)) {               // registers -> ring slot m & 1
+    auto store_row = [&](int m, auto nvc) __attribute__((always_inline)) {     // registers -> ring slot m & 1
+        constexpr int NV = decltype(nvc)::value;
+        static_assert(NV >= 0 && NV <= 63, "vector-memory counter range");
         if (stager) {
+            asm volatile("s_waitcnt vmcnt(%8)"
+                         : "+v"(stg[0]), "+v"(stg[1]), "+v"(stg[2]), "+v"(stg[3]), "+v"(stg[4]), "+v"(stg[5]),
+                           "+v"(stg[6]), "+v"(stg[7])
+                         : "n"(NV));
+            uint4 in8[8];
+#pragma unroll
+            for (int p = 0; p < 8; ++p) in8[p] = make_uint4(stg[p].x, stg[p].y, stg[p].z, stg[p].w);
             uint4 t[8];
-            roll_transpose8x8(stg, t);
+            roll_transpose8x8(in8, t);
             uint16_t* dst = lds + (m & 1) * ROWSZ + (pg * 8) * PS + cg8 * 8;
 #pragma unroll
             for (int p = 0; p < 8; ++p) *reinterpret_cast<uint4*>(dst + p * PS) = t[p];
@@ -269,7 +285,7 @@ __global__ __launch_bounds__(kRThreads, 1) void igemm_roll_kernel(IgemmArgs a) {
     });
     __syncthreads();   // the image space becomes the input ring
 
-    store_row(0);
+    store_row(0, std::integral_constant<int, 0>{});
     __syncthreads();
 
     // ---- outputs: buffer stores over the block's OBT channel planes of this sample
@@ -357,7 +373,16 @@ __global__ __launch_bounds__(kRThreads, 1) void igemm_roll_kernel(IgemmArgs a) {
                     mfma_xw<(f < NAG), (b == 0)>(acc[J][ob], Bq[x % NQ], Wf[ob][s * CG + cg]);
                 });
             }
-            if constexpr (LD && x == STAGE_X) store_row(j + 1);
+            if constexpr (LD && x == STAGE_X) {
+                // stores issued since the loads: those riding MFMAs 0 .. MX-1
+                constexpr int MX = (x < NA ? x + 1 : NA) * NIMM * NOB;
+                constexpr int NV = [] {
+                    int c = 0;
+                    for (int i = 0; i < NST; ++i) c += (ST && i * AVAIL / NST < MX) ? 1 : 0;
+                    return c;
+                }();
+                store_row(j + 1, std::integral_constant<int, NV>{});
+            }
         });
         // the set finishing in this step (row j - TR + 1) is stored in the next one
         roll_drain(acc[(J + 1) % NSETS]);
