@@ -28,7 +28,7 @@
 // scalar registers) at device scope: outputs are written once.
 //
 // The plan admits whole segments only (rows_per_seg divides Uo, 128-column
-// strips tile Vo, 64-channel blocks tile Cout), so no store needs a mask.
+// strips tile Vo, 32- or 64-filter blocks tile Cout), so no store needs a mask.
 // NM = rows_per_seg mod TR fixes, at compile time, which register set each
 // step of the segment's tail uses.
 #include <hip/hip_runtime.h>
@@ -429,7 +429,11 @@ __global__ __launch_bounds__(kRThreads, 1) void igemm_roll_kernel(IgemmArgs a) {
 
 // ---------------------------------------------------------------- planning
 
-static bool roll_shape(int NOB, int TR, int TS, int CG) { return NOB == 2 && TR == 3 && TS == 3 && CG == 4; }
+// instantiated shapes: 3x3 with 64 channels and 64-filter blocks; 5x5 with
+// 32 channels and 32-filter blocks
+static bool roll_shape(int NOB, int TR, int TS, int CG) {
+    return (NOB == 2 && TR == 3 && TS == 3 && CG == 4) || (NOB == 1 && TR == 5 && TS == 5 && CG == 2);
+}
 
 static int roll_lds(int NOB, int TR, int TS, int CG) {
     const int CIN = CG * 16, PS = 8 * ((CIN / 8) | 1), RPX8 = (kRStrip + TS - 1 + 7) / 8;
@@ -446,9 +450,9 @@ static int roll_lds(int NOB, int TR, int TS, int CG) {
 // splits into whole strips and equal row segments.
 bool igemm_roll_plan(IgemmArgs& a) {
     if (a.bp || a.istr != 1 || a.ostr != 1 || a.oph_r != 0 || a.oph_c != 0) return false;
-    if (a.Cin % 16 != 0 || a.Cout % 64 != 0 || a.Vo % kRStrip != 0) return false;
+    if (a.Cin % 16 != 0 || a.Cout % 32 != 0 || a.Vo % kRStrip != 0) return false;
     if (a.base_c % 8 != 0 || a.in_pitch % 8 != 0 || a.Tr != a.R || a.Ts != a.S) return false;
-    const int NOB = 2, CG = a.Cin / 16;
+    const int NOB = a.Cout % 64 == 0 ? 2 : 1, CG = a.Cin / 16;
     if (!roll_shape(NOB, a.Tr, a.Ts, CG)) return false;
     if (a.wmode == 0 && !(a.wr0 == 0 && a.wrstep == 1 && a.ws0 == 0 && a.wsstep == 1)) return false;
     if (a.wmode == 1 && !(a.wr0 == a.R - 1 && a.wrstep == -1 && a.ws0 == a.S - 1 && a.wsstep == -1))
@@ -464,7 +468,7 @@ bool igemm_roll_plan(IgemmArgs& a) {
     if (lds > device_lds_limit()) return false;
     // equal segments of at least TR rows, about 256 workgroups
     a.nvb = a.Vo / kRStrip;
-    const int strips = a.ntiles * a.Nn * a.nvb * (a.Cout / 64);
+    const int strips = a.ntiles * a.Nn * a.nvb * (a.Cout / (32 * NOB));
     int best = 0;
     for (int rps = a.Tr; rps <= a.Uo; ++rps) {
         if (a.Uo % rps != 0) continue;
@@ -474,7 +478,7 @@ bool igemm_roll_plan(IgemmArgs& a) {
     if (best == 0) return false;
     a.rows_per_seg = best;
     a.nseg = a.Uo / best;
-    a.OB = 64;
+    a.OB = 32 * NOB;
     a.wvec = 1;
     a.phase = 0;
     a.lds_bytes = lds;
@@ -490,7 +494,7 @@ static hipError_t launch_roll(const IgemmArgs& a, hipStream_t s) {
                                            hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
         if (e != hipSuccess) return e;
     }
-    dim3 grid(a.ntiles * a.Nn * a.nvb * a.nseg, a.Cout / 64);
+    dim3 grid(a.ntiles * a.Nn * a.nvb * a.nseg, a.Cout / (32 * NOB));
     hipLaunchKernelGGL(k, grid, dim3(kRThreads), a.lds_bytes, s, a);
     return hipGetLastError();
 }
@@ -502,6 +506,15 @@ hipError_t launch_igemm_roll(const IgemmArgs& a, hipStream_t s) {
             case 0: return launch_roll<2, 3, 3, 4, 0>(a, s);
             case 1: return launch_roll<2, 3, 3, 4, 1>(a, s);
             default: return launch_roll<2, 3, 3, 4, 2>(a, s);
+        }
+    }
+    if (a.OB == 32 && a.Tr == 5 && a.Ts == 5 && CG == 2 && a.rows_per_seg >= 5) {
+        switch (a.rows_per_seg % 5) {
+            case 0: return launch_roll<1, 5, 5, 2, 0>(a, s);
+            case 1: return launch_roll<1, 5, 5, 2, 1>(a, s);
+            case 2: return launch_roll<1, 5, 5, 2, 2>(a, s);
+            case 3: return launch_roll<1, 5, 5, 2, 3>(a, s);
+            default: return launch_roll<1, 5, 5, 2, 4>(a, s);
         }
     }
     return hipErrorInvalidValue;

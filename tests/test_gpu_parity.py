@@ -110,6 +110,10 @@ SMALL = {
     # and input gradient (segments of 4 rows: rows mod 3 = 1; of 3 rows: = 0)
     "roll_bf16": Layer("roll_bf16", 1, 64, 64, 256, 256, 3, 3, 1, 1, 1, 2, 1, "bf16", "uniform", 101),
     "roll96_bf16": Layer("roll96_bf16", 2, 64, 64, 96, 128, 3, 3, 1, 1, 1, 1, 1, "bf16", "uniform", 102),
+    # 32 channels and filters, 5x5: the rolling-row kernel with five live
+    # output rows (segments of 8 rows: rows mod 5 = 3; of 5 rows: = 0)
+    "roll5_bf16": Layer("roll5_bf16", 1, 32, 32, 256, 256, 5, 5, 1, 2, 1, 2, 2, "bf16", "uniform", 103),
+    "roll5b_bf16": Layer("roll5b_bf16", 2, 32, 32, 80, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 104),
 }
 
 
@@ -160,7 +164,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
                                   "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16",
                                   "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16", "bp7_bf16", "bp3_bf16",
-                                  "roll_bf16", "roll96_bf16"])
+                                  "roll_bf16", "roll96_bf16", "roll5_bf16", "roll5b_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
