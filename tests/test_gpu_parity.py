@@ -114,6 +114,12 @@ SMALL = {
     # output rows (segments of 8 rows: rows mod 5 = 3; of 5 rows: = 0)
     "roll5_bf16": Layer("roll5_bf16", 1, 32, 32, 256, 256, 5, 5, 1, 2, 1, 2, 2, "bf16", "uniform", 103),
     "roll5b_bf16": Layer("roll5b_bf16", 2, 32, 32, 80, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 104),
+    # the remaining tails: 3x3 segments of 5 rows (mod 3 = 2); 5x5 segments
+    # of 6, 7 and 9 rows (mod 5 = 1, 2, 4)
+    "roll50_bf16": Layer("roll50_bf16", 1, 64, 64, 50, 128, 3, 3, 1, 1, 1, 1, 1, "bf16", "uniform", 105),
+    "roll5c_bf16": Layer("roll5c_bf16", 1, 32, 32, 96, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 106),
+    "roll5d_bf16": Layer("roll5d_bf16", 1, 32, 32, 112, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 107),
+    "roll5e_bf16": Layer("roll5e_bf16", 1, 32, 32, 81, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 108),
 }
 
 
@@ -164,7 +170,8 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
 @pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5a_s", "c5b_s", "s2k7_f32", "c3a_s",
                                   "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16",
                                   "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16", "bp7_bf16", "bp3_bf16",
-                                  "roll_bf16", "roll96_bf16", "roll5_bf16", "roll5b_bf16"])
+                                  "roll_bf16", "roll96_bf16", "roll5_bf16", "roll5b_bf16",
+                                  "roll50_bf16", "roll5c_bf16", "roll5d_bf16", "roll5e_bf16"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
