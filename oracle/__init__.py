@@ -23,7 +23,9 @@ What it computes (Dryden et al., arXiv 1903.06681):
 Parity notes: the convolution functions are pinned by the tests in
 ``tests/test_oracle.py`` (hand cases, a library convolution, finite
 differences, the adjoint identity, exact integer arithmetic and the
-decomposition invariant); the halo functions by brute-force index checks.
+decomposition invariant); the sampled-point functions by bit-identity with
+the whole-tensor ones at random, first and last flat indices; the halo
+functions by brute-force index checks.
 """
 from __future__ import annotations
 
@@ -165,11 +167,6 @@ def conv_bwd_filter_points(x, dy, R, S, stride, pad, flat_idx) -> np.ndarray:
 def round_f32(a: np.ndarray) -> np.ndarray:
     """Round fp64 results once to fp32, to nearest-even."""
     return np.asarray(a, np.float64).astype(np.float32)
-
-
-def flops(N, C, K, Ho, Wo, R, S) -> int:
-    """Multiply-adds counted as 2 flops, padding taps included, per pass."""
-    return 2 * N * K * C * R * S * Ho * Wo
 
 
 # --------------------------------------------------------------------------

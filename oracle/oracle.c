@@ -10,17 +10,18 @@
  * Notation (paper -> here): N samples, C channels, F filters -> K,
  * filter K x K -> R x S, stride S -> stride, padding P -> pad.
  *
- * The paper states Eqs. (1)-(3) for stride 1 and "same" padding and says both
- * assumptions are inessential.  The general form used here is the one those
- * equations reduce to at stride 1, pad = floor(K/2):
+ * The paper states Eqs. (1)-(3) for stride 1 and output-preserving padding
+ * and notes that neither assumption matters to the method.  The general form
+ * used here is the one those equations reduce to at stride 1,
+ * pad = floor(K/2):
  *
  *   y [n,k,p,q] = sum_c sum_r sum_s  X(n,c, p*stride-pad+r, q*stride-pad+s) * w[k,c,r,s]
  *   dx[n,c,i,j] = sum_k sum_r sum_s  DY(n,k, (i+pad-r)/stride, (j+pad-s)/stride) * w[k,c,r,s]
  *                 (a term exists only where both divisions are exact)
  *   dw[k,c,r,s] = sum_n sum_p sum_q  dy[n,k,p,q] * X(n,c, p*stride-pad+r, q*stride-pad+s)
  *
- * X and DY read zero outside the tensor (the paper: out-of-range subscripts
- * are handled by padding).  There is no filter flip (Eq. (1) pairs x at
+ * X and DY read zero outside the tensor (Sec. II-A leaves subscripts outside
+ * the tensor to the padding).  There is no filter flip (Eq. (1) pairs x at
  * offset +a with w at a+O) and no bias.
  *
  * Arithmetic: inputs are fp32 arrays (bf16 inputs arrive already widened,

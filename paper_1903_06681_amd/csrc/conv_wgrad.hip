@@ -71,6 +71,12 @@ struct Plan {
 // tap-split kernel: square filters whose R*S taps spread over four waves fit
 // the accumulators (at most 14 tiles of 32x32 per wave)
 static bool taps_filter(int R, int S) { return R == S && R >= 2 && R <= 7; }
+// stride-2 tap-split kernel: instantiated phase filters (ceil(R/2) of 2 to 4,
+// square), i.e. filters of 3 x 3 to 8 x 8
+static bool taps2_filter(int R, int S) {
+    const int rp = (R + 1) / 2, sp = (S + 1) / 2;
+    return rp == sp && rp >= 2 && rp <= 4;
+}
 
 // k-slice kernel geometry (kernel below)
 template <int NW>
@@ -122,8 +128,7 @@ static bool make_plan(int dtype, int ntiles, int N, int C, int K, int R, int S, 
                       int Hot, int Wot, int base_c, int dy_off, Plan* pl) {
     std::memset(pl, 0, sizeof(*pl));
     const bool xcol_aligned = base_c % 8 == 0;   // strip staging reads whole 16-byte x chunks
-    const bool phase2 = dtype == 1 && stride == 2 && 4 * C <= 32 && xcol_aligned &&
-                        taps_filter((R + 1) / 2, (S + 1) / 2);
+    const bool phase2 = dtype == 1 && stride == 2 && 4 * C <= 32 && xcol_aligned && taps2_filter(R, S);
     if ((dtype == 1 && stride == 1 && S <= 7 && xcol_aligned) || phase2) {
         int qw = kBQ;   // strip width
         if (phase2) {

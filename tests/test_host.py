@@ -169,3 +169,18 @@ def test_status_strings():
         s = dc.lib().dc_status_string(code)
         assert isinstance(s, bytes) and len(s) > 0
     assert dc.lib().dc_status_string(-99) == b"unknown status"
+
+
+def test_bwd_filter_plans_only_instantiated_stride2_filters():
+    """Stride-2 bf16 layers with at most 8 channels go to the phase-image
+    tap-split kernel only when their phase filter (ceil(R/2) square) has an
+    instantiation (2 to 4); a 9 x 9 stride-2 layer has none and must be
+    rejected on the host with DC_ERR_UNSUPPORTED, not fail at launch."""
+    ok = prob(N=1, C=3, K=8, H=32, W=32, R=7, S=7, stride=2, pad=3, P=1, Q=1, halo=3,
+              dtype=dc.DC_BF16)
+    assert dc.bwd_filter_workspace_bytes(ok, 0) > 0
+    big = prob(N=1, C=3, K=8, H=32, W=32, R=9, S=9, stride=2, pad=4, P=1, Q=1, halo=4,
+               dtype=dc.DC_BF16)
+    assert dc.lib().dc_validate(ctypes.byref(big), 0) == 0
+    assert dc.bwd_filter_workspace_bytes(big, 0) == 0
+    assert _status(dc.conv_bwd_filter, big, 0, A16, A32, A48, 0, _FakeWs(A16, 1 << 20), 0) == -5

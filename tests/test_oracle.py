@@ -311,3 +311,63 @@ def test_decomposed_stride_equals_undecomposed(P, Q, h, R, pad, stride, kind):
         ulp = np.abs(np.spacing(dw0))
         assert np.all(np.abs(dw0.astype(np.float64) - dw1) <= ulp)
 
+
+
+# ------------------------------------------------- sampled-point entry points
+
+POINT_CASES = [
+    # N, C, K, H, W, R, S, stride, pad: non-square, N > 1, 1x1, 5x5, 7x7,
+    # stride 2, several pads, R != S
+    (3, 2, 5, 7, 9, 3, 3, 1, 1),
+    (2, 3, 2, 6, 5, 1, 1, 1, 0),
+    (2, 2, 3, 9, 8, 5, 5, 1, 2),
+    (2, 3, 4, 11, 10, 7, 7, 2, 3),
+    (1, 2, 3, 9, 7, 3, 3, 2, 1),
+    (2, 2, 3, 10, 9, 3, 3, 2, 0),
+    (3, 2, 2, 6, 8, 3, 5, 1, 0),
+    (2, 4, 3, 8, 11, 5, 3, 1, 2),
+]
+
+
+def _point_indices(rng, size, n_rand=40):
+    """Index 0, the last index and random indices in between."""
+    return np.unique(np.concatenate([[0, size - 1], rng.integers(0, size, n_rand)])).astype(np.int64)
+
+
+@pytest.mark.parametrize("case", POINT_CASES)
+def test_sampled_points_equal_whole_tensor_outputs(case):
+    """conv_*_points decode each flat index into (n, k|c, p|i, q|j) or
+    (k, c, r, s) on their own; every sampled value must be bit-identical to
+    the same element of the whole-tensor result (pinned above against a
+    library convolution, finite differences and the adjoint identity) and
+    agree with fp64 torch conv2d and its autograd to rounding.  A wrong decode
+    order or extent (rows for columns, C for K, R for S) fails here."""
+    N, C, K, H, W, R, S, st, pad = case
+    rng = np.random.default_rng(abs(hash(case)) % 2**32)
+    x = _rand(rng, (N, C, H, W))
+    w = _rand(rng, (K, C, R, S))
+    y = orc.conv_fwd(x, w, st, pad)
+    dy = _rand(rng, y.shape)
+    dx = orc.conv_bwd_data(dy, w, H, W, st, pad)
+    dw = orc.conv_bwd_filter(x, dy, R, S, st, pad)
+    xt = torch.from_numpy(x.astype(np.float64)).requires_grad_(True)
+    wt = torch.from_numpy(w.astype(np.float64)).requires_grad_(True)
+    yt = F.conv2d(xt, wt, stride=st, padding=pad)
+    yt.backward(torch.from_numpy(dy.astype(np.float64)))
+    for full, lib, pts_fn in (
+            (y, yt.detach().numpy(), lambda i: orc.conv_fwd_points(x, w, st, pad, i)),
+            (dx, xt.grad.numpy(), lambda i: orc.conv_bwd_data_points(dy, w, H, W, st, pad, i)),
+            (dw, wt.grad.numpy(), lambda i: orc.conv_bwd_filter_points(x, dy, R, S, st, pad, i))):
+        idx = _point_indices(rng, full.size)
+        got = pts_fn(idx)
+        assert np.array_equal(got, full.reshape(-1)[idx])
+        np.testing.assert_allclose(got, lib.reshape(-1)[idx], rtol=1e-12, atol=1e-12)
+        # every element once, in a shuffled order
+        perm = rng.permutation(full.size).astype(np.int64)
+        assert np.array_equal(pts_fn(perm), full.reshape(-1)[perm])
+
+
+def test_sampled_points_of_empty_request():
+    x = np.ones((1, 1, 4, 4), np.float32)
+    w = np.ones((1, 1, 3, 3), np.float32)
+    assert orc.conv_fwd_points(x, w, 1, 1, np.zeros(0, np.int64)).shape == (0,)
