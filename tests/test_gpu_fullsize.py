@@ -1,0 +1,170 @@
+"""GPU checks at the benchmark's full sizes that the sampled parity cases do
+not reach on their own:
+
+* halo pack/unpack of the whole 4x4 grid of the large layers, bit-exact
+  against the oracle's halo index sets (Sec. III-A) -- a c5a plane carries
+  1,028 halo elements and a c4 plane 2,052, more than one pass of a
+  256-thread workgroup;
+* the weight gradient of the benchmark's c5a tile (k-slice kernel, dy rows
+  that start on the margin column) with NaN in every dy margin: dw is
+  bit-identical to the run with real margins (it reads no dy halo, Sec.
+  III-A) and to a second run (fixed-order reduction);
+* the benchmark's two-stream step (the dy halo exchange beside the weight
+  gradient, Sec. IV-A) equals the one-stream step bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import harness as H
+import oracle as orc
+import paper_1903_06681_amd as dc
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+X, DY, ALL = dc.DC_X, dc.DC_DY, dc.DC_ALL_TILES
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _bits(t):
+    return t.view(torch.int16 if t.element_size() == 2 else torch.int32)
+
+
+@pytest.mark.parametrize("name", ["c5a", "c4", "c5b"])
+@pytest.mark.parametrize("which", [X, DY])
+def test_halo_full_size_all_tiles_bit_exact(name, which):
+    L = wl.LAYERS[name]
+    p = dc.Problem.of(L)
+    nt = L.P * L.Q
+    print(f"[halo full] {name} {'x' if which == X else 'dy'}", flush=True)
+    g = wl.draw(L, "x" if which == X else "dy")
+    tw = L.Wt if which == X else L.Wot
+    h = L.halo
+    tiles = H.alloc_tiles(p, which, nt, L.dtype)
+    H.scatter_interiors(tiles, H.to_device(g, L.dtype), p, which)
+    hel = dc.halo_elems(p, which)
+    sentinel = -3.0
+    send = torch.full((nt, hel), sentinel, dtype=H.TORCH_DT[L.dtype], device="cuda")
+    dc.halo_pack(p, ALL, which, tiles, send)
+    dc.halo_unpack(p, ALL, which, send, tiles)
+    torch.cuda.synchronize()
+    for t in range(nt):
+        ti, tj = divmod(t, L.Q)
+        ref = np.full(hel, sentinel, np.float32)
+        orc.halo_pack(g, L.P, L.Q, ti, tj, h, ref)
+        rb = _bits(H.to_device(ref, L.dtype))
+        bad = int((_bits(send[t]) != rb).sum())
+        assert bad == 0, f"pack tile {t}: {bad} mismatches"
+        win = H.to_device(orc.tile_window(g, L.P, L.Q, ti, tj, h), L.dtype)
+        got = tiles[t][:, :, :, :tw + 2 * h].contiguous()
+        bad = int((_bits(got) != _bits(win)).sum())
+        assert bad == 0, f"unpack tile {t}: {bad} mismatches"
+        assert bool(torch.isnan(tiles[t][:, :, :, tw + 2 * h:].float()).all()), "pitch padding written"
+        del win, got
+
+
+def _tile_setup(L, tile):
+    """The benchmark's single-tile inputs: padded x and dy tiles with their
+    halos filled through pack (all tiles) -> exchange -> unpack (this tile)."""
+    p = dc.Problem.of(L)
+    nt = L.P * L.Q
+    tdt = H.TORCH_DT[L.dtype]
+    x, w, dy = wl.draw(L, "x"), wl.draw(L, "w"), wl.draw(L, "dy")
+    xt = H.alloc_tiles(p, X, nt, L.dtype)
+    H.scatter_interiors(xt, H.to_device(x, L.dtype), p, X)
+    sx = torch.empty((nt, dc.halo_elems(p, X)), dtype=tdt, device="cuda")
+    dc.halo_pack(p, ALL, X, xt, sx)
+    rx = torch.zeros_like(sx[0])
+    H.exchange_into(rx, sx, p, X, tile)
+    xp = xt[tile].clone()
+    del xt
+    dyt = H.alloc_tiles(p, DY, nt, L.dtype)
+    H.scatter_interiors(dyt, H.to_device(dy, L.dtype), p, DY)
+    sy = torch.empty((nt, dc.halo_elems(p, DY)), dtype=tdt, device="cuda")
+    dc.halo_pack(p, ALL, DY, dyt, sy)
+    ry = torch.zeros_like(sy[0])
+    H.exchange_into(ry, sy, p, DY, tile)
+    dyp_nan = dyt[tile].clone()          # dy margins still NaN
+    del dyt
+    dyp = dyp_nan.clone()
+    dc.halo_unpack(p, tile, X, rx, xp)
+    dc.halo_unpack(p, tile, DY, ry, dyp)
+    return p, H.to_device(w, L.dtype), xp, dyp, dyp_nan, rx, ry
+
+
+def test_full_size_bwd_filter_reads_no_dy_halo():
+    L = wl.LAYERS["c5a"]
+    tile = 5
+    print("[kslice nan-margin] c5a tile 5", flush=True)
+    p, wd, xp, dyp, dyp_nan, _, _ = _tile_setup(L, tile)
+    ws = torch.empty(dc.bwd_filter_workspace_bytes(p, tile), dtype=torch.uint8, device="cuda")
+    dws = [torch.empty((L.K, L.C, L.R, L.S), device="cuda") for _ in range(3)]
+    dc.conv_bwd_filter(p, tile, xp, dyp, dws[0], 0, ws)
+    dc.conv_bwd_filter(p, tile, xp, dyp_nan, dws[1], 0, ws)
+    dc.conv_bwd_filter(p, tile, xp, dyp_nan, dws[2], 0, ws)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(dws[1]).all())
+    assert torch.equal(_bits(dws[0]), _bits(dws[1]))
+    assert torch.equal(_bits(dws[1]), _bits(dws[2]))
+
+
+def test_two_stream_step_equals_one_stream_step():
+    """The dy pack/unpack on a second stream beside the weight gradient, the
+    input gradient after both (the benchmark's overlapped schedule), gives
+    the outputs of the same calls on one stream, bit for bit, over several
+    back-to-back steps."""
+    L = wl.LAYERS["c5a"]
+    tile = 5
+    print("[two-stream step] c5a tile 5", flush=True)
+    p, wd, xp, dyp, dyp_nan, rx, ry = _tile_setup(L, tile)
+    sx, sy = torch.empty_like(rx), torch.empty_like(ry)
+    y = torch.empty((L.N, L.K, L.Hot, L.Wot), device="cuda")
+    dx = torch.empty((L.N, L.C, L.Ht, L.Wt), device="cuda")
+    dw = torch.empty((L.K, L.C, L.R, L.S), device="cuda")
+    ws = torch.empty(dc.bwd_filter_workspace_bytes(p, tile), dtype=torch.uint8, device="cuda")
+    sa = torch.cuda.current_stream()
+    sb = torch.cuda.Stream()   # default priority
+    ev_f, ev_d = torch.cuda.Event(), torch.cuda.Event()
+
+    def serial():
+        dc.halo_pack(p, tile, X, xp, sx)
+        dc.halo_unpack(p, tile, X, rx, xp)
+        dc.conv_fwd(p, tile, xp, wd, y)
+        dc.halo_pack(p, tile, DY, dyp, sy)
+        dc.halo_unpack(p, tile, DY, ry, dyp)
+        dc.conv_bwd_filter(p, tile, xp, dyp, dw, 0, ws)
+        dc.conv_bwd_data(p, tile, dyp, wd, dx)
+
+    def overlapped():
+        dc.halo_pack(p, tile, X, xp, sx, sa)
+        dc.halo_unpack(p, tile, X, rx, xp, sa)
+        dc.conv_fwd(p, tile, xp, wd, y, sa)
+        ev_f.record(sa)
+        sb.wait_event(ev_f)
+        dc.halo_pack(p, tile, DY, dyp_nan, sy, sb)
+        dc.halo_unpack(p, tile, DY, ry, dyp_nan, sb)
+        ev_d.record(sb)
+        dc.conv_bwd_filter(p, tile, xp, dyp_nan, dw, 0, ws, sa)
+        sa.wait_event(ev_d)
+        dc.conv_bwd_data(p, tile, dyp_nan, wd, dx, sa)
+
+    serial()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (y, dx, dw, sx, sy)]
+    for it in range(4):
+        for t in (y, dx, dw, sx, sy):
+            t.fill_(float("nan"))
+        overlapped()
+        torch.cuda.synchronize()
+        for k, (a, b) in enumerate(zip((y, dx, dw, sx, sy), ref)):
+            assert torch.equal(_bits(a), _bits(b)), (it, ("y", "dx", "dw", "send_x", "send_dy")[k])
+    # the margins the second stream filled equal the one-stream ones
+    assert torch.equal(_bits(dyp_nan), _bits(dyp))

@@ -333,10 +333,13 @@ def test_stale_hip_error_of_the_caller_is_not_reported():
     _check("dw", dw.cpu().numpy(), dwr, L.dtype)
 
 
-def test_bwd_filter_ignores_dy_halo_and_is_deterministic():
+@pytest.mark.parametrize("name", ["c5a_s", "kslice_bf16", "kslice_p0_bf16", "taps5_bf16", "c4_s"])
+def test_bwd_filter_ignores_dy_halo_and_is_deterministic(name):
     """dw needs no dy halo (Sec. III-A): NaN in every dy margin must not reach
-    dw.  Two runs give identical bits (fixed-order reduction, no atomics)."""
-    L = SMALL["c5a_s"]
+    dw.  Two runs give identical bits (fixed-order reduction, no atomics).
+    kslice_* run the k-slice kernel, whose 16-byte dy loads start on the
+    margin column."""
+    L = SMALL[name]
     p = dc.Problem.of(L)
     nt = L.P * L.Q
     x, w, dy = wl.draw(L, "x"), wl.draw(L, "w"), wl.draw(L, "dy")
@@ -359,12 +362,36 @@ def test_bwd_filter_ignores_dy_halo_and_is_deterministic():
 
 # ------------------------------------------------------------------ full size
 
-def _sample_idx(rng, shape, region, n_rand, edges=True):
+def _seam_lines(lo, hi, period):
+    """Lines lo <= v < hi on either side of every multiple of `period` past lo."""
+    out = []
+    for m in range(lo + period, hi, period):
+        out += [m - 1, m]
+    return np.array(out, np.int64)
+
+
+def _sample_idx(rng, shape, region, n_rand, edges=True, seams=True):
     """Flat indices into a tensor of `shape` = [A, B, rows, cols], restricted to
-    rows/cols in region=(r0, r1, c0, c1), including the region's border lines."""
+    rows/cols in region=(r0, r1, c0, c1), including the region's border lines
+    and, with seams, the lines on both sides of every 8-row boundary (row
+    segments of the rolling-row and k-slice kernels) and every 64-column
+    boundary (64- and 128-column strips), where work passes from one
+    workgroup to the next."""
     A, B, Hh, Ww = shape
     r0, r1, c0, c1 = region
     pts = []
+    if seams:
+        sr, sc = _seam_lines(r0, r1, 8), _seam_lines(c0, c1, 64)
+        m = n_rand // 4
+        if sr.size:
+            pts.append(np.stack([rng.integers(0, A, m), rng.integers(0, B, m),
+                                 rng.choice(sr, m), rng.integers(c0, c1, m)], 1))
+        if sc.size:
+            pts.append(np.stack([rng.integers(0, A, m), rng.integers(0, B, m),
+                                 rng.integers(r0, r1, m), rng.choice(sc, m)], 1))
+        if sr.size and sc.size:
+            pts.append(np.stack([rng.integers(0, A, m), rng.integers(0, B, m),
+                                 rng.choice(sr, m), rng.choice(sc, m)], 1))
     a = rng.integers(0, A, n_rand)
     b = rng.integers(0, B, n_rand)
     r = rng.integers(r0, r1, n_rand)
