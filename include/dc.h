@@ -145,6 +145,24 @@ dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Allocation-free weight gradient, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Same operation, arguments, kernels and results as
+ * dc_conv_bwd_filter, without a workspace argument: the chunk partials live
+ * in a fixed device array of DC_BWD_FILTER_NOALLOC_MAX_BYTES that the library
+ * holds on every GPU it runs on until the process ends (its address is looked
+ * up on the first call on a device).  Returns DC_ERR_WORKSPACE, launching
+ * nothing, when dc_bwd_filter_workspace_bytes(prob, tile) exceeds that size.
+ * Calls no hipMalloc, hipFree or allocating routine.  Every call on one GPU
+ * shares that GPU's array: calls that overlap on one GPU (two streams, two
+ * host threads) race and must be serialised by the caller.
+ */
+#define DC_BWD_FILTER_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+dc_status dc_conv_bwd_filter_noalloc(const dc_problem* prob, int32_t tile, const void* x_pad,
+                                     const void* dy_pad, float* dw, int32_t accumulate,
+                                     void* stream);
+
+/*
  * Halo pack (Sec. III-A; message terms of Sec. V-A): copy the h-wide bands of
  * the owned block of t_pad (which = DC_X: an x tile; DC_DY: a dy tile) that
  * each existing neighbour needs into the send buffer.  Reads only the owned

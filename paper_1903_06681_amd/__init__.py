@@ -31,6 +31,8 @@ _lib = ctypes.CDLL(LIB_PATH)
 DC_F32, DC_BF16 = 0, 1
 DC_X, DC_DY = 0, 1
 DC_ALL_TILES = -1
+# capacity of the fixed workspace of dc_conv_bwd_filter_noalloc (include/dc.h)
+BWD_FILTER_NOALLOC_MAX_BYTES = 64 << 20
 
 STATUS = {
     0: "DC_OK", -1: "DC_ERR_NULL", -2: "DC_ERR_SHAPE", -3: "DC_ERR_DTYPE", -4: "DC_ERR_HALO",
@@ -40,7 +42,7 @@ STATUS = {
 
 EXPORTS = (
     "dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_halo_pack", "dc_halo_unpack",
-    "dc_validate", "dc_tile_pitch", "dc_tile_elems", "dc_halo_elems",
+    "dc_conv_bwd_filter_noalloc", "dc_validate", "dc_tile_pitch", "dc_tile_elems", "dc_halo_elems",
     "dc_bwd_filter_workspace_bytes", "dc_required_halo", "dc_tile_dims", "dc_status_string",
 )
 
@@ -73,6 +75,7 @@ _I = ctypes.c_int32
 _lib.dc_conv_fwd.argtypes = [_P, _I, _V, _V, _V, _V]
 _lib.dc_conv_bwd_data.argtypes = [_P, _I, _V, _V, _V, _V]
 _lib.dc_conv_bwd_filter.argtypes = [_P, _I, _V, _V, _V, _I, _V, ctypes.c_size_t, _V]
+_lib.dc_conv_bwd_filter_noalloc.argtypes = [_P, _I, _V, _V, _V, _I, _V]
 _lib.dc_halo_pack.argtypes = [_P, _I, _I, _V, _V, _V]
 _lib.dc_halo_unpack.argtypes = [_P, _I, _I, _V, _V, _V]
 _lib.dc_validate.argtypes = [_P, _I]
@@ -88,7 +91,8 @@ _lib.dc_required_halo.argtypes = [_P, _I, ctypes.POINTER(_I)]
 _lib.dc_tile_dims.argtypes = [_P, ctypes.POINTER(_I)]
 _lib.dc_status_string.argtypes = [_I]
 _lib.dc_status_string.restype = ctypes.c_char_p
-for _n in ("dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_halo_pack",
+for _n in ("dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_conv_bwd_filter_noalloc",
+           "dc_halo_pack",
            "dc_halo_unpack", "dc_validate", "dc_required_halo", "dc_tile_dims"):
     getattr(_lib, _n).restype = ctypes.c_int32
 
@@ -181,6 +185,13 @@ def conv_bwd_filter(prob, tile, x_pad, dy_pad, dw, accumulate, workspace, stream
     _check(_lib.dc_conv_bwd_filter(ctypes.byref(prob), tile, _ptr(x_pad), _ptr(dy_pad),
                                    _ptr(dw), accumulate, _ptr(workspace), ws_bytes,
                                    _stream(stream)), "dc_conv_bwd_filter")
+
+
+def conv_bwd_filter_noalloc(prob, tile, x_pad, dy_pad, dw, accumulate, stream=None):
+    """Eq. (2) on a tile with the library's fixed device workspace (no allocation)."""
+    _check(_lib.dc_conv_bwd_filter_noalloc(ctypes.byref(prob), tile, _ptr(x_pad), _ptr(dy_pad),
+                                           _ptr(dw), accumulate, _stream(stream)),
+           "dc_conv_bwd_filter_noalloc")
 
 
 def halo_pack(prob, tile, which, t_pad, send, stream=None):

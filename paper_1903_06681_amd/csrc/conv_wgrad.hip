@@ -29,6 +29,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 
 #include "bf16util.h"
 #include "kernels.h"
@@ -1576,6 +1577,40 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(unsigned((a.F + 63) / 64)), dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- fixed workspace
+
+// Chunk partials of dc_conv_bwd_filter_noalloc: a file-scope device array
+// instead of a caller's buffer, for callers that cannot allocate.  Each GPU
+// holds its own copy until the process ends.  Host code must never pass the
+// array's name to a kernel (on the host it is only a stand-in for the symbol):
+// the device address comes from hipGetSymbolAddress, once per device, with
+// that device current.  The kernels write every partial they later read, so
+// nothing in it has to start at zero.
+static constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+size_t wgrad_scratch_capacity() { return kScratchBytes; }
+
+hipError_t wgrad_scratch_ptr(void** ptr) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace dc

@@ -399,20 +399,28 @@ size_t dc_bwd_filter_workspace_bytes(const dc_problem* prob, int32_t tile) {
                                  g.h - g.pad, g.h);
 }
 
-dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x_pad,
-                             const void* dy_pad, float* dw, int32_t accumulate,
-                             void* workspace, size_t workspace_bytes, void* stream) {
-    Geo g;
-    dc_status st = make_geo_tile(prob, tile, &g);
+}  // extern "C"
+
+namespace dc {
+
+// Checks shared by both weight-gradient entry points; *need = workspace bytes.
+static dc_status bwd_filter_check(const dc_problem* prob, int32_t tile, const void* x_pad,
+                                  const void* dy_pad, const float* dw, int32_t accumulate, Geo* g,
+                                  size_t* need) {
+    dc_status st = make_geo_tile(prob, tile, g);
     if (st != DC_OK) return st;
     if (accumulate != 0 && accumulate != 1) return DC_ERR_ARG;
     if (!x_pad || !dy_pad || !dw) return DC_ERR_NULL;
     if (misaligned(x_pad) || misaligned(dy_pad) || misaligned(dw)) return DC_ERR_ALIGN;
+    const int nt = tile == DC_ALL_TILES ? g->ntiles : 1;
+    *need = wgrad_workspace_bytes(g->dtype, nt, g->N, g->C, g->K, g->R, g->S, g->stride, g->Hot,
+                                  g->Wot, g->h - g->pad, g->h);
+    return DC_OK;
+}
+
+static dc_status bwd_filter_launch(const Geo& g, int32_t tile, const void* x_pad, const void* dy_pad,
+                                   float* dw, int32_t accumulate, void* workspace, void* stream) {
     const int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
-    size_t need = wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot,
-                                 g.h - g.pad, g.h);
-    if (need > 0 && (!workspace || workspace_bytes < need)) return DC_ERR_WORKSPACE;
-    if (need > 0 && misaligned(workspace)) return DC_ERR_ALIGN;
     WgradArgs a;
     std::memset(&a, 0, sizeof(a));
     a.x = x_pad; a.dy = dy_pad; a.part = static_cast<float*>(workspace); a.dw = dw;
@@ -428,6 +436,35 @@ dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x
     if (!wgrad_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
     clear_stale_error();
     return launched(launch_wgrad(a, g.dtype, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace dc
+
+extern "C" {
+
+dc_status dc_conv_bwd_filter(const dc_problem* prob, int32_t tile, const void* x_pad,
+                             const void* dy_pad, float* dw, int32_t accumulate,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+    Geo g;
+    size_t need = 0;
+    dc_status st = bwd_filter_check(prob, tile, x_pad, dy_pad, dw, accumulate, &g, &need);
+    if (st != DC_OK) return st;
+    if (need > 0 && (!workspace || workspace_bytes < need)) return DC_ERR_WORKSPACE;
+    if (need > 0 && misaligned(workspace)) return DC_ERR_ALIGN;
+    return bwd_filter_launch(g, tile, x_pad, dy_pad, dw, accumulate, workspace, stream);
+}
+
+dc_status dc_conv_bwd_filter_noalloc(const dc_problem* prob, int32_t tile, const void* x_pad,
+                                     const void* dy_pad, float* dw, int32_t accumulate,
+                                     void* stream) {
+    Geo g;
+    size_t need = 0;
+    dc_status st = bwd_filter_check(prob, tile, x_pad, dy_pad, dw, accumulate, &g, &need);
+    if (st != DC_OK) return st;
+    if (need > wgrad_scratch_capacity()) return DC_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if (need > 0 && wgrad_scratch_ptr(&ws) != hipSuccess) return DC_ERR_HIP;
+    return bwd_filter_launch(g, tile, x_pad, dy_pad, dw, accumulate, ws, stream);
 }
 
 }  // extern "C"

@@ -135,4 +135,10 @@ size_t wgrad_workspace_bytes(int dtype, int ntiles, int N, int C, int K, int R, 
 bool wgrad_plan(WgradArgs& a, int dtype);
 hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s);
 
+// Fixed device workspace of the allocation-free weight-gradient entry point:
+// its capacity in bytes, and its address on the current device (looked up
+// once per device, on the first call there).
+size_t wgrad_scratch_capacity();
+hipError_t wgrad_scratch_ptr(void** ptr);
+
 }  // namespace dc

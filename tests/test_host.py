@@ -184,3 +184,19 @@ def test_bwd_filter_plans_only_instantiated_stride2_filters():
     assert dc.lib().dc_validate(ctypes.byref(big), 0) == 0
     assert dc.bwd_filter_workspace_bytes(big, 0) == 0
     assert _status(dc.conv_bwd_filter, big, 0, A16, A32, A48, 0, _FakeWs(A16, 1 << 20), 0) == -5
+
+
+def test_noalloc_bwd_filter_limit_matches_header_and_rejects_larger_problems():
+    hdr = open(os.path.join(ROOT, "include", "dc.h")).read()
+    m = re.search(r"#define\s+DC_BWD_FILTER_NOALLOC_MAX_BYTES\s+\(\(size_t\)(\d+)\s*<<\s*(\d+)\)", hdr)
+    assert m and int(m.group(1)) << int(m.group(2)) == dc.BWD_FILTER_NOALLOC_MAX_BYTES
+    # 1024 samples of a 56x56 3x3 layer: the partials exceed the fixed array;
+    # rejected on the host before the device is touched
+    big = prob(N=1024, C=64, K=64, H=56, W=56, P=1, Q=1, dtype=dc.DC_BF16)
+    assert dc.bwd_filter_workspace_bytes(big, 0) > dc.BWD_FILTER_NOALLOC_MAX_BYTES
+    st = dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(big), 0, A16, A32, A48, 0, None)
+    assert st == -6
+    p = prob()
+    assert dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(p), 0, A16, A32, A48, 2, None) == -10
+    assert dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(p), 0, A16, None, A48, 0, None) == -1
+    assert dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(p), 0, A16, A32, MIS, 0, None) == -7
