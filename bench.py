@@ -10,21 +10,26 @@ per-tile shape in the workload set.
 One step = the whole per-tile path of Sec. III-A on that tile:
   halo pack x -> halo unpack x -> forward (Eq. 1) ->
   halo pack dy -> halo unpack dy -> weight gradient (Eq. 2) -> input gradient (Eq. 3)
-with the dy halo pack/unpack on a second stream beside the weight gradient
-(which needs no dy halo); the input gradient waits for both.  The same step
-with every call on one stream is timed too, eagerly and as a replayed HIP
-graph (each replay checked bit for bit against the eager step first), and
-the fastest schedule is the step (field overlap.step_schedule): on one GPU
-the pack and unpack kernels compete for the CUs the weight gradient fills.
-The neighbours' halo regions (what the exchange would deliver) are prepared
-once before timing; the transport itself is not part of a GPU's compute.
-All inputs are resident in device memory when timing starts.
+timed on one stream, with the dy halo pack/unpack on a second stream beside
+the weight gradient (which needs no dy halo; the input gradient waits for
+both), and as a replayed HIP graph of the one-stream step (each replay checked
+bit for bit against the eager step first); the fastest schedule is the step
+(field overlap.step_schedule).  The neighbours' halo regions (what the
+exchange would deliver) are prepared once before timing; the transport itself
+is not part of a GPU's compute.  All inputs are resident in device memory
+when timing starts.
 
 value = (forward + backward-data + backward-filter flops) / step time, TFLOP/s,
 with the step time from K whole steps between two events.  Each pass is then
-timed on its own (K back-to-back calls between two events on the launch
-stream); `roofline` reports the slowest convolution pass against its bound.
-Prints one JSON line.  Only one GPU is supported (--gpus 1).
+timed on its own, warm (K back-to-back calls on the same inputs between two
+events on the launch stream) and cold (K back-to-back calls, each on its own
+copy of the inputs, the copies together larger than the 256 MB Infinity
+Cache, after a 512 MB flush: the same dispatch amortisation as the warm
+reading, with inputs that come from HBM).  `roofline` reports the slowest
+convolution pass (warm) against its bound.  Every workload's single-tile
+passes are timed too (field `workloads`), as are the halo calls of the whole
+grid by band class (N/S rows, W/E columns and corners).  Prints one JSON
+line.  Only one GPU is supported (--gpus 1).
 """
 import argparse
 import json
@@ -39,24 +44,28 @@ METRIC = "conv fwd+bwd TFLOP/s and % MFMA peak per layer tile on 1 MI355X; halo 
 PEAK = {"bf16_tflops": 2516.6, "f32_tflops": 157.3, "hbm_gbps": 8000.0}
 
 
-def algorithmic(L):
+def algorithmic(L, bx, by):
     """Compulsory HBM bytes and flops per launch of each pass on one tile.
 
-    Inputs in the layer dtype (x tile including its real halo margins, dy
-    interior, w), outputs in fp32, each read or written once."""
+    Inputs in the layer dtype (x tile including its real halo bands, dy
+    interior, w), outputs in fp32, each read or written once.  bx, by: halo
+    band widths (above, below, left, right) of x and dy; an interior tile
+    receives all of them."""
     e = 2 if L.dtype == "bf16" else 4
-    h = L.halo
-    # real halo = margins that come from neighbours (interior tile: all four sides)
-    x_in = L.N * L.C * (L.Ht + 2 * h) * (L.Wt + 2 * h) * e
-    dy_in = L.N * L.K * (L.Hot + 2 * h) * (L.Wot + 2 * h) * e
+    x_in = L.N * L.C * (L.Ht + bx[0] + bx[1]) * (L.Wt + bx[2] + bx[3]) * e
+    dy_in = L.N * L.K * (L.Hot + by[0] + by[1]) * (L.Wot + by[2] + by[3]) * e
     dy_int = L.N * L.K * L.Hot * L.Wot * e
     w = L.K * L.C * L.R * L.S * e
     y = L.N * L.K * L.Hot * L.Wot * 4
     dx = L.N * L.C * L.Ht * L.Wt * 4
     dw = L.K * L.C * L.R * L.S * 4
     flops = L.flops_per_pass_tile()
-    hx = L.N * L.C * (2 * h * (L.Ht + L.Wt) + 4 * h * h) * e
-    hy = L.N * L.K * (2 * h * (L.Hot + L.Wot) + 4 * h * h) * e
+
+    def ring(b, th, tw):
+        return (b[0] + b[1]) * tw + th * (b[2] + b[3]) + (b[0] + b[1]) * (b[2] + b[3])
+
+    hx = L.N * L.C * ring(bx, L.Ht, L.Wt) * e
+    hy = L.N * L.K * ring(by, L.Hot, L.Wot) * e
     return {
         "fwd": {"flops": flops, "bytes": x_in + w + y},
         "bwd_data": {"flops": flops, "bytes": dy_in + w + dx},
@@ -68,17 +77,26 @@ def algorithmic(L):
     }
 
 
-def halo_payload_bytes(L):
-    """Bytes a pack of the whole grid sends: the real halo regions of every tile."""
+BAND_DIRS = {1: ((-1, 0), (1, 0)), 2: ((0, -1), (0, 1)),
+             4: ((-1, -1), (-1, 1), (1, -1), (1, 1))}
+
+
+def halo_payload_bytes(L, bx, band_mask=7):
+    """Bytes a pack of the whole grid sends for x: the band of every region
+    whose receiving neighbour exists, restricted to the band classes of
+    band_mask (1 N/S rows, 2 W/E columns, 4 corners)."""
     e = 2 if L.dtype == "bf16" else 4
-    h, tot = L.halo, 0
-    for ti in range(L.P):
-        for tj in range(L.Q):
-            for di in (-1, 0, 1):
-                for dj in (-1, 0, 1):
-                    if (di, dj) == (0, 0) or not (0 <= ti + di < L.P and 0 <= tj + dj < L.Q):
-                        continue
-                    tot += L.N * L.C * (h if di else L.Ht) * (h if dj else L.Wt) * e
+    rows = {-1: bx[1], 0: L.Ht, 1: bx[0]}     # sent north: the neighbour's rows below, ...
+    cols = {-1: bx[3], 0: L.Wt, 1: bx[2]}
+    tot = 0
+    for m, dirs in BAND_DIRS.items():
+        if not band_mask & m:
+            continue
+        for ti in range(L.P):
+            for tj in range(L.Q):
+                for di, dj in dirs:
+                    if 0 <= ti + di < L.P and 0 <= tj + dj < L.Q:
+                        tot += L.N * L.C * rows[di] * cols[dj] * e
     return tot
 
 
@@ -94,6 +112,21 @@ def source_digest():
             with open(os.path.join(d, f), "rb") as fh:
                 hsh.update(fh.read())
     return hsh.hexdigest()
+
+
+def traffic_summary(name):
+    """key: value lines of a committed counter summary (profiles/<name>.txt),
+    or None when it is missing or was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{name}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith(("#", " ", "|", "`")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    return kv if kv.get("source_sha256") == source_digest() else None
 
 
 def measured_traffic(kernel, workload, tile):
@@ -165,14 +198,62 @@ def cpu_baseline(L, x, w, dy, tile, seconds):
         counts[kind] = n
         total_flops += n * per
         total_t += dt
-    return {
+    out = {
         "value": total_flops / total_t / 1e12,
         "unit": "TFLOP/s",
         "cores": orc.num_threads(),
         "kind": "oracle",
         "sample": (f"{counts['y']} y, {counts['dx']} dx and {counts['dw']} dw outputs of tile "
                    f"({ti},{tj}), fp64 direct loops, {total_t:.1f} s"),
+        "cpu_model": cpu_model(),
+        "affinity_cores": len(os.sched_getaffinity(0)),
     }
+    out["small_configs"] = small_config_oracle_times()
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def small_config_oracle_times():
+    """The oracle's three whole passes on the two small configurations (the
+    undecomposed 32x32 layer and the same layer on a 2x2 grid, i.e. the
+    undecomposed computation of its 32x32 image), at one thread and at all
+    threads: GFLOP/s per pass."""
+    import oracle as orc
+    import workloads as wl
+
+    res = {}
+    nthreads = orc.num_threads()
+    for name in ("c1", "c2"):
+        L = wl.LAYERS[name]
+        x, w, dy = wl.draw(L, "x"), wl.draw(L, "w"), wl.draw(L, "dy")
+        fl = 2 * L.N * L.K * L.C * L.R * L.S * L.Ho * L.Wo
+        d = {}
+        for th in (1, nthreads):
+            orc.set_num_threads(th)
+            t = {}
+            for k, f in (("fwd", lambda: orc.conv_fwd(x, w, L.stride, L.pad)),
+                         ("bwd_data", lambda: orc.conv_bwd_data(dy, w, L.H, L.W, L.stride, L.pad)),
+                         ("bwd_filter", lambda: orc.conv_bwd_filter(x, dy, L.R, L.S, L.stride, L.pad))):
+                f()
+                reps, t0 = 0, time.perf_counter()
+                while time.perf_counter() - t0 < 0.3:
+                    f()
+                    reps += 1
+                t[k] = round(fl * reps / (time.perf_counter() - t0) / 1e9, 3)
+            d[f"GFLOP/s_{th}_threads"] = t
+        res[name] = d
+    orc.set_num_threads(nthreads)
+    return res
 
 
 def all_workloads(steps):
@@ -199,9 +280,10 @@ def all_workloads(steps):
         calls = {"fwd": lambda: dc.conv_fwd(p, tile, xp, w, y),
                  "bwd_data": lambda: dc.conv_bwd_data(p, tile, dyp, w, dx),
                  "bwd_filter": lambda: dc.conv_bwd_filter(p, tile, xp, dyp, dw, 0, ws)}
-        alg = algorithmic(L)
+        alg = algorithmic(L, dc.halo_bands(p, dc.DC_X), dc.halo_bands(p, dc.DC_DY))
         peak = PEAK["bf16_tflops"] if L.dtype == "bf16" else PEAK["f32_tflops"]
-        d = {"desc": L.desc, "tile": tile}
+        d = {"desc": L.desc, "tile": tile, "dtype": L.dtype,
+             "peak_TFLOP/s": peak}
         for k, f in calls.items():
             for _ in range(3):
                 f()
@@ -217,7 +299,7 @@ def all_workloads(steps):
             roof = min(peak, a["flops"] / a["bytes"] * PEAK["hbm_gbps"] / 1e3)
             tf = a["flops"] / (ms * 1e-3) / 1e12
             d[k] = {"ms": round(ms, 5), "TFLOP/s": round(tf, 2), "roof_TFLOP/s": round(roof, 1),
-                    "pct_roof": round(100 * tf / roof, 2)}
+                    "pct_roof": round(100 * tf / roof, 2), "pct_peak": round(100 * tf / peak, 2)}
         res[name] = d
         del xp, dyp, y, dx, ws
     return res
@@ -247,9 +329,12 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="skip the graph-replayed step")
     ap.add_argument("--cpu-seconds", type=float, default=24.0)
     ap.add_argument("--no-cold", action="store_true",
-                    help="skip the cold timings (each step or pass after a 512 MB cache flush)")
-    ap.add_argument("--all-workloads", action="store_true",
-                    help="also time every workload's single-tile passes (field 'workloads')")
+                    help="skip the cold timings (passes and step over copies of the inputs larger "
+                         "than the Infinity Cache)")
+    ap.add_argument("--cold-copies", type=int, default=8,
+                    help="input copies the cold timings cycle through")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the single-tile passes of every workload (field 'workloads')")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB a few times (the known-size "
                          "kernel against which HBM byte counters are scaled) and exit")
@@ -448,7 +533,8 @@ def main():
         torch.cuda.synchronize()
         per_call[n] = e0.elapsed_time(e1) / args.steps
 
-    alg = algorithmic(L)
+    bx, by = dc.halo_bands(p, X), dc.halo_bands(p, DY)
+    alg = algorithmic(L, bx, by)
     flops_step = 3 * L.flops_per_pass_tile()
     value = flops_step / (ms_per_step * 1e-3) / 1e12
     peak_tf = PEAK["bf16_tflops"] if L.dtype == "bf16" else PEAK["f32_tflops"]
@@ -507,13 +593,19 @@ def main():
         "setup_s": round(t_setup, 1),
     }
 
-    # halo pack / unpack of the whole grid in one launch each (all tiles)
-    payload = halo_payload_bytes(L)
+    # halo pack / unpack of the whole grid in one launch each (all tiles), by
+    # band class: N/S rows (contiguous), W/E columns and corners (one element
+    # per row of a plane), and all of them
     sx_grid = torch.empty((nt, max(dc.halo_elems(p, X), 1)), dtype=tdt, device=dev)
-    grid_calls = {"pack_x_all_tiles": lambda: dc.halo_pack(p, dc.DC_ALL_TILES, X, xt, sx_grid, sh),
-                  "unpack_x_all_tiles": lambda: dc.halo_unpack(p, dc.DC_ALL_TILES, X, sx_grid, xt, sh)}
     grid = {}
-    for n, c in grid_calls.items():
+    classes = {"ns": dc.DC_BAND_NS, "we_corners": dc.DC_BAND_WE | dc.DC_BAND_CORNERS, "all": dc.DC_BAND_ALL}
+    grid_calls = {}
+    for cname, mask in classes.items():
+        grid_calls[f"pack_x_all_tiles_{cname}"] = (
+            mask, lambda m=mask: dc.halo_pack_bands(p, dc.DC_ALL_TILES, X, m, xt, sx_grid, sh))
+        grid_calls[f"unpack_x_all_tiles_{cname}"] = (
+            mask, lambda m=mask: dc.halo_unpack_bands(p, dc.DC_ALL_TILES, X, m, sx_grid, xt, sh))
+    for n, (mask, c) in grid_calls.items():
         c()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -523,8 +615,17 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         warm = e0.elapsed_time(e1) / args.steps
-        grid[n] = {"payload_bytes": payload, "ms": round(warm, 5),
-                   "useful_GB/s": round(2 * payload / (warm * 1e-3) / 1e9, 1)}
+        payload = halo_payload_bytes(L, bx, mask)
+        d = {"payload_bytes": payload, "ms": round(warm, 5),
+             "useful_GB/s": round(2 * payload / (warm * 1e-3) / 1e9, 1)}
+        kv = traffic_summary(f"dc_halo_{L.name}_all_tiles_traffic")
+        key = n.replace("_x_all_tiles", "")
+        if kv and f"{key}_dram_bytes" in kv:
+            dram = float(kv[f"{key}_dram_bytes"])
+            d["dram_bytes"] = int(dram)
+            d["dram_GB/s"] = round(dram / (warm * 1e-3) / 1e9, 1)
+            d["dram_over_useful"] = round(dram / (2 * payload), 2)
+        grid[n] = d
     out["halo_all_tiles"] = grid
     out["overlap"] = {"serial_step_ms": round(serial_ms, 5), "overlapped_step_ms": round(overlapped_ms, 5),
                       "graph_step_ms": None if graph_ms is None else round(graph_ms, 5),
@@ -532,44 +633,68 @@ def main():
                       "what": "dy halo pack/unpack on a second stream beside the weight gradient"}
 
     if not args.no_cold:
-        # Cold timings: a 512 MB write (more than the 256 MB Infinity Cache and
-        # the L2s) before each timed interval, outside it.  A single launch
-        # between two events also pays one dispatch, so cold pass times sit a
-        # few microseconds above the back-to-back ones.
+        # Cold timings: K back-to-back calls (or steps), call i on its own copy
+        # of the tile inputs; the K copies together exceed the 256 MB Infinity
+        # Cache, and a 512 MB write before the timed interval evicts the
+        # setup's traces, so every call reads its inputs from HBM while the
+        # dispatch is amortised exactly as in the warm reading.
+        K = max(2, args.cold_copies)
+        xs = [xp.clone() for _ in range(K)]
+        dys = [dyp.clone() for _ in range(K)]
+        rxs = [recv_x.clone() for _ in range(K)]
+        rys = [recv_dy.clone() for _ in range(K)]
+        copy_bytes = K * (xp.numel() + dyp.numel()) * xp.element_size()
         flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+        cold_calls = {
+            "pack_x": lambda i: dc.halo_pack(p, tile, X, xs[i], send_x, sh),
+            "unpack_x": lambda i: dc.halo_unpack(p, tile, X, rxs[i], xs[i], sh),
+            "fwd": lambda i: dc.conv_fwd(p, tile, xs[i], wd, y, sh),
+            "pack_dy": lambda i: dc.halo_pack(p, tile, DY, dys[i], send_dy, sh),
+            "unpack_dy": lambda i: dc.halo_unpack(p, tile, DY, rys[i], dys[i], sh),
+            "bwd_filter": lambda i: dc.conv_bwd_filter(p, tile, xs[i], dys[i], dw, 0, ws, sh),
+            "bwd_data": lambda i: dc.conv_bwd_data(p, tile, dys[i], wd, dx, sh),
+        }
 
-        def cold_ms(fn, reps):
+        def cold_ms(fn, reps=3):
             ts = []
             for _ in range(reps):
                 flush.zero_()
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-                fn()
+                for i in range(K):
+                    fn(i)
                 e1.record(stream)
                 torch.cuda.synchronize()
-                ts.append(e0.elapsed_time(e1))
+                ts.append(e0.elapsed_time(e1) / K)
             return {"mean": round(float(np.mean(ts)), 5), "std": round(float(np.std(ts)), 5),
-                    "min": round(float(np.min(ts)), 5), "runs": reps}
+                    "min": round(float(np.min(ts)), 5), "runs": reps, "calls_per_run": K}
 
-        reps = max(3, min(args.steps, 10))
-        out["cold_step_ms"] = cold_ms(step, reps)
-        for n, c in zip(names, calls):
-            cm = cold_ms(c, reps)
+        for n in names:
+            cm = cold_ms(cold_calls[n])
             passes[n]["cold_ms"] = cm
-            if alg[n]["flops"]:
-                passes[n]["cold_TFLOP/s"] = round(alg[n]["flops"] / (cm["mean"] * 1e-3) / 1e12, 2)
-            passes[n]["cold_GB/s"] = round(alg[n]["bytes"] / (cm["mean"] * 1e-3) / 1e9, 1)
-        for n, c in grid_calls.items():
-            cm = cold_ms(c, reps)
-            grid[n]["cold_ms"] = cm
-            grid[n]["cold_useful_GB/s"] = round(2 * payload / (cm["mean"] * 1e-3) / 1e9, 1)
+            a_ = alg[n]
+            if a_["flops"]:
+                tf = a_["flops"] / (cm["mean"] * 1e-3) / 1e12
+                ai = a_["flops"] / a_["bytes"]
+                roof = min(peak_tf, ai * PEAK["hbm_gbps"] / 1e3)
+                passes[n]["cold_TFLOP/s"] = round(tf, 2)
+                passes[n]["cold_pct_roof"] = round(100 * tf / roof, 2)
+            passes[n]["cold_GB/s"] = round(a_["bytes"] / (cm["mean"] * 1e-3) / 1e9, 1)
 
-        del flush
+        def cold_step(i):
+            for n in names:
+                cold_calls[n](i)
+
+        out["cold_step_ms"] = cold_ms(cold_step)
+        out["cold_protocol"] = (f"{K} calls per timed run, call i on input copy i "
+                                f"({copy_bytes / 2**20:.0f} MiB of x and dy tiles), after a 512 MB write")
+        del flush, xs, dys, rxs, rys
+
+    if not args.no_workloads:
+        out["workloads"] = all_workloads(args.steps)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, x, w, dy, tile, args.cpu_seconds)
-    if args.all_workloads:
-        out["workloads"] = all_workloads(args.steps)
     print(json.dumps(out), flush=True)
 
 

@@ -53,17 +53,20 @@ def gather_outputs(out_tiles: torch.Tensor, prob, which_out: str) -> torch.Tenso
     return g
 
 
-def region_table(prob, which):
-    """(offset, rows, cols) of each packed region, in the interface's fixed order."""
+def region_table(prob, which, send=False):
+    """(offset, rows, cols) of each packed region, in the interface's fixed
+    order: receive regions have the shape of the tile's margin bands, send
+    regions that of the neighbour's opposite margin band."""
     Ht, Wt, Hot, Wot = dc.tile_dims(prob)
     th, tw = (Ht, Wt) if which == dc.DC_X else (Hot, Wot)
     ch = prob.C if which == dc.DC_X else prob.K
-    h = prob.halo
-    sizes = {"N": (h, tw), "S": (h, tw), "W": (th, h), "E": (th, h),
-             "NW": (h, h), "NE": (h, h), "SW": (h, h), "SE": (h, h)}
+    bn, bs, bw, be = dc.halo_bands(prob, which)
+    rows = {-1: bn, 0: th, 1: bs}
+    cols = {-1: bw, 0: tw, 1: be}
     table, off = {}, 0
     for d in DIRS:
-        r, c = sizes[d]
+        di, dj = STEP[OPP[d]] if send else STEP[d]
+        r, c = rows[di], cols[dj]
         table[d] = (off, r, c)
         off += prob.N * ch * r * c
     return table
@@ -81,12 +84,13 @@ def exchange_into(recv: torch.Tensor, sends: torch.Tensor, prob, which, t):
     """Emulated transport for tile t: recv region d <- neighbour d's region opposite(d).
     sends: [ntiles, halo_elems] packed buffers of all tiles; recv: [halo_elems]."""
     table = region_table(prob, which)
+    stable = region_table(prob, which, send=True)
     for d in DIRS:
         nb = neighbour(prob, t, d)
         if nb is None:
             continue
         off, r, c = table[d]
-        ooff = table[OPP[d]][0]
+        ooff = stable[OPP[d]][0]
         ch = prob.C if which == dc.DC_X else prob.K
         n = prob.N * ch * r * c
         recv[off:off + n].copy_(sends[nb, ooff:ooff + n])

@@ -63,7 +63,8 @@ typedef enum { DC_X = 0, DC_DY = 1 } dc_which;       /* which tensor a tile/halo
  * Wo * stride = W (stride 1: "same" output), and Ho % P = Wo % Q = 0, so that
  * a tile owns exactly the outputs whose taps start in its input block.  At
  * stride > 1 a tile may need no halo on one side (e.g. 3x3 stride 2 pad 1: x
- * 1 below, 0 above); the one width h still serves every side.
+ * 1 below, 0 above): the layout keeps the margin h on every side, and the
+ * halo calls move only the band each side needs (dc_halo_bands).
  *
  * halo is the margin width h kept on every side of every tile (for both the x
  * and the dy tile).  It must be at least what each pass reads beyond the tile
@@ -90,21 +91,39 @@ typedef struct {
  *   dx     [N][C][Ht][Wt]     fp32
  *   dw     [K][C][R][S]       fp32
  * pitch = dc_tile_pitch(): at least width+2h, rounded up to 16 bytes.  Pitch
- * columns beyond width+2h are never read or written.
+ * columns beyond width+2h are never written; kernels may read them (as part
+ * of an aligned 16-byte access), and their values never reach a result.
  *
  * Tiles are numbered tile = ti*Q + tj, ti = 0..P-1 top to bottom, tj = 0..Q-1
  * left to right.  With tile = DC_ALL_TILES every per-tile buffer argument
  * (tile, send/recv, y, dx) is an array of P*Q consecutive per-tile buffers in
  * tile order, and one launch serves the whole grid.
  *
+ * Halo bands (Sec. III-A).  A tile's margin ring is supplied by its eight
+ * neighbours; the band from each side is as wide as the passes read on that
+ * side (dc_halo_bands: rows above bN, below bS, columns left bW, right bE;
+ * all equal to h for the usual stride-1 "same" layers).  Margin cells outside
+ * the bands, and bands whose neighbour does not exist, hold zeros after
+ * unpack: the convolution's zero padding.
+ *
  * Packed halo buffers (send/recv) hold eight regions, in the order
- * N, S, W, E, NW, NE, SW, SE, each laid out [N][channels][rows][cols], at fixed
- * offsets given by the nominal sizes N,S: h x Wt;  W,E: Ht x h;  corners h x h
+ * N, S, W, E, NW, NE, SW, SE, each laid out [N][channels][rows][cols].
+ * Region d of a RECV buffer holds the band of margin d: N bN x Wt, S bS x Wt,
+ * W Ht x bW, E Ht x bE, NW bN x bW, NE bN x bE, SW bS x bW, SE bS x bE
  * (output-tile extents Hot, Wot for dy).  Region d of a SEND buffer holds the
- * band of the owned block that the neighbour in direction d needs; region d of
- * a RECV buffer holds what that neighbour sent (its region opposite to d).
- * Total elements per tile: dc_halo_elems().
+ * band of the owned block that the neighbour in direction d receives, i.e.
+ * the shape of that neighbour's margin opposite to d (S for d = N, ...).
+ * Regions follow each other without gaps; the two layouts have the same
+ * total.  dc_halo_elems() is that total rounded up to a multiple of 16 bytes
+ * (the padding at the end is never written), so the consecutive buffers of an
+ * all-tiles call each start 16-byte aligned.
  */
+
+/* band classes of the margin ring, for dc_halo_pack_bands / dc_halo_unpack_bands */
+#define DC_BAND_NS      1   /* rows above and below the owned block (regions N, S) */
+#define DC_BAND_WE      2   /* columns left and right of it (regions W, E) */
+#define DC_BAND_CORNERS 4   /* the four corner blocks (regions NW, NE, SW, SE) */
+#define DC_BAND_ALL     7
 
 /* ---- the five operations ---- */
 
@@ -163,24 +182,39 @@ dc_status dc_conv_bwd_filter_noalloc(const dc_problem* prob, int32_t tile, const
                                      void* stream);
 
 /*
- * Halo pack (Sec. III-A; message terms of Sec. V-A): copy the h-wide bands of
- * the owned block of t_pad (which = DC_X: an x tile; DC_DY: a dy tile) that
- * each existing neighbour needs into the send buffer.  Reads only the owned
- * block; writes only regions whose neighbour exists.  Bitwise copy.
+ * Halo pack (Sec. III-A; message terms of Sec. V-A): copy the bands of the
+ * owned block of t_pad (which = DC_X: an x tile; DC_DY: a dy tile) that each
+ * existing neighbour needs into the send buffer.  Reads only the owned block
+ * (and pitch columns, see above); writes only regions whose neighbour
+ * exists.  Bitwise copy.
  */
 dc_status dc_halo_pack(const dc_problem* prob, int32_t tile, int32_t which,
                        const void* t_pad, void* send, void* stream);
 
 /*
- * Halo unpack (Sec. III-A): write the eight h-wide margins of t_pad.  Margin d
- * receives region d of recv when the neighbour in direction d exists, and
- * zeros (the convolution's zero padding; Sec. II-A) when it does not.  Writes
- * only margins, never the owned block.  With tile = DC_ALL_TILES, recv is the
+ * Halo unpack (Sec. III-A): write the whole h-wide margin ring of t_pad.  The
+ * band of margin d receives region d of recv when the neighbour in direction
+ * d exists; every other margin cell becomes zero (the convolution's zero
+ * padding, Sec. II-A, and margin beyond the band widths).  Writes only
+ * margins, never the owned block.  With tile = DC_ALL_TILES, recv is the
  * array of all tiles' SEND buffers and each margin is read directly from the
  * neighbour's opposite region: that read is the emulated exchange.
  */
 dc_status dc_halo_unpack(const dc_problem* prob, int32_t tile, int32_t which,
                          const void* recv, void* t_pad, void* stream);
+
+/*
+ * dc_halo_pack / dc_halo_unpack restricted to some band classes (bands: an OR
+ * of DC_BAND_*; DC_BAND_ALL is the full call): pack writes only the regions of
+ * those classes, unpack writes only the margin cells of those classes.  Lets
+ * a caller move the contiguous N/S rows and the strided W/E columns at
+ * different times (or time them apart).  DC_ERR_ARG for an empty or unknown
+ * mask.
+ */
+dc_status dc_halo_pack_bands(const dc_problem* prob, int32_t tile, int32_t which, int32_t bands,
+                             const void* t_pad, void* send, void* stream);
+dc_status dc_halo_unpack_bands(const dc_problem* prob, int32_t tile, int32_t which, int32_t bands,
+                               const void* recv, void* t_pad, void* stream);
 
 /* ---- host-only helpers (no GPU needed) ---- */
 
@@ -193,7 +227,7 @@ int64_t dc_tile_pitch(const dc_problem* prob, int32_t which);
 /* Elements of one padded x or dy tile ([N][ch][rows+2h][pitch]); -1 if invalid. */
 int64_t dc_tile_elems(const dc_problem* prob, int32_t which);
 
-/* Elements of one tile's packed halo buffer for x or dy; -1 if invalid. */
+/* Elements of one tile's packed halo buffer for x or dy (16-byte multiple); -1 if invalid. */
 int64_t dc_halo_elems(const dc_problem* prob, int32_t which);
 
 /* Workspace bytes dc_conv_bwd_filter needs for this tile argument (0 if none). */
@@ -206,6 +240,14 @@ size_t dc_bwd_filter_workspace_bytes(const dc_problem* prob, int32_t tile);
  * the dy rows the input gradient reads.  Same in both spatial dimensions.
  */
 dc_status dc_required_halo(const dc_problem* prob, int32_t which, int32_t lohi[2]);
+
+/*
+ * Band widths the halo calls move for x (which = DC_X) or dy (DC_DY):
+ * bw = {rows above, rows below, columns left, columns right} of a tile, the
+ * margins the passes read (x: forward and weight gradient, Eq. (1)/(2);
+ * dy: input gradient, Eq. (3)).  Each is at most the problem's halo.
+ */
+dc_status dc_halo_bands(const dc_problem* prob, int32_t which, int32_t bw[4]);
 
 /* Tile extents: dims = {Ht, Wt, Hot, Wot}. */
 dc_status dc_tile_dims(const dc_problem* prob, int32_t dims[4]);

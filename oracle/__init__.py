@@ -62,6 +62,8 @@ def _load():
         getattr(lib, name).restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     _lib = lib
     return lib
 
@@ -69,6 +71,11 @@ def _load():
 def num_threads() -> int:
     """OpenMP threads the oracle's loops run on."""
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Run the oracle's loops on n threads from now on."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def _f32(a) -> np.ndarray:
@@ -189,22 +196,33 @@ def owned_ranges(H, W, P, Q, ti, tj):
     return (ti * Ht, ti * Ht + Ht - 1), (tj * Wt, tj * Wt + Wt - 1)
 
 
-def window_ranges(H, W, P, Q, ti, tj, h):
-    """Owned block widened by h on every side (global indices, inclusive)."""
+def _bands(h, bw):
+    """Band widths (above, below, left, right); None means h on every side."""
+    return (h, h, h, h) if bw is None else tuple(int(v) for v in bw)
+
+
+def window_ranges(H, W, P, Q, ti, tj, h, bw=None):
+    """Owned block widened by its halo bands (global indices, inclusive): h on
+    every side, or bw = (above, below, left, right)."""
+    a, b, l, r = _bands(h, bw)
     (qh, rh), (qw, rw) = owned_ranges(H, W, P, Q, ti, tj)
-    return (qh - h, rh + h), (qw - h, rw + h)
+    return (qh - a, rh + b), (qw - l, rw + r)
 
 
-def tile_window(g: np.ndarray, P, Q, ti, tj, h) -> np.ndarray:
-    """Owned block of tile (ti,tj) plus its h-wide halo, read from the global
-    tensor g [N,C,H,W]; halo elements outside the domain are zero."""
+def tile_window(g: np.ndarray, P, Q, ti, tj, h, bw=None) -> np.ndarray:
+    """Owned block of tile (ti,tj) plus an h-wide margin, read from the global
+    tensor g [N,C,H,W]; margin cells outside the domain are zero, and so are
+    cells outside the halo bands bw = (above, below, left, right) when given
+    (the part of the margin no pass reads)."""
     N, C, H, W = g.shape
     (a0, a1), (b0, b1) = window_ranges(H, W, P, Q, ti, tj, h)
+    (qa, qb), (ql, qr) = window_ranges(H, W, P, Q, ti, tj, h, bw)
     out = np.zeros((N, C, a1 - a0 + 1, b1 - b0 + 1), g.dtype)
-    for i in range(a0, a1 + 1):
+    for i in range(max(a0, qa), min(a1, qb) + 1):
         if 0 <= i < H:
-            lo, hi = max(b0, 0), min(b1, W - 1)
-            out[:, :, i - a0, lo - b0:hi - b0 + 1] = g[:, :, i, lo:hi + 1]
+            lo, hi = max(b0, ql, 0), min(b1, qr, W - 1)
+            if lo <= hi:
+                out[:, :, i - a0, lo - b0:hi - b0 + 1] = g[:, :, i, lo:hi + 1]
     return out
 
 
@@ -220,16 +238,24 @@ def _intersect(a, b):
     return (lo, hi) if lo <= hi else None
 
 
-def region_shapes(Ht, Wt, h):
-    """Nominal (rows, cols) of each packed region."""
-    return {"N": (h, Wt), "S": (h, Wt), "W": (Ht, h), "E": (Ht, h),
-            "NW": (h, h), "NE": (h, h), "SW": (h, h), "SE": (h, h)}
+def region_shapes(Ht, Wt, h, bw=None, send=False):
+    """(rows, cols) of each packed region.  A receive region d is the band of
+    margin d; a send region d is what the neighbour in direction d receives,
+    the band of ITS margin opposite to d."""
+    a, b, l, r = _bands(h, bw)
+    rows = {-1: a, 0: Ht, 1: b}
+    cols = {-1: l, 0: Wt, 1: r}
+    out = {}
+    for d in DIRECTIONS:
+        di, dj = STEP[OPPOSITE[d]] if send else STEP[d]
+        out[d] = (rows[di], cols[dj])
+    return out
 
 
-def region_offsets(N, Cc, Ht, Wt, h):
+def region_offsets(N, Cc, Ht, Wt, h, bw=None, send=False):
     """Element offset of each region in one tile's packed buffer, and the total."""
     offs, o = {}, 0
-    for d, (r, c) in region_shapes(Ht, Wt, h).items():
+    for d, (r, c) in region_shapes(Ht, Wt, h, bw, send).items():
         offs[d] = o
         o += N * Cc * r * c
     return offs, o
@@ -241,7 +267,7 @@ def neighbour(P, Q, ti, tj, d):
     return (ni, nj) if (0 <= ni < P and 0 <= nj < Q) else None
 
 
-def pack_region_ranges(H, W, P, Q, ti, tj, h, d):
+def pack_region_ranges(H, W, P, Q, ti, tj, h, d, bw=None):
     """Global index ranges that tile (ti,tj) sends toward direction d: the part
     of its owned block lying in the neighbour's halo window.  None if no
     neighbour exists (nothing is sent)."""
@@ -249,56 +275,69 @@ def pack_region_ranges(H, W, P, Q, ti, tj, h, d):
     if nb is None:
         return None
     own_h, own_w = owned_ranges(H, W, P, Q, ti, tj)
-    win_h, win_w = window_ranges(H, W, P, Q, nb[0], nb[1], h)
-    return _intersect(own_h, win_h), _intersect(own_w, win_w)
+    win_h, win_w = window_ranges(H, W, P, Q, nb[0], nb[1], h, bw)
+    rh, rw = _intersect(own_h, win_h), _intersect(own_w, win_w)
+    if rh is None or rw is None:
+        return (0, -1), (0, -1)   # an empty band
+    return rh, rw
 
 
-def halo_pack(g: np.ndarray, P, Q, ti, tj, h, send: np.ndarray) -> np.ndarray:
+def halo_pack(g: np.ndarray, P, Q, ti, tj, h, send: np.ndarray, bw=None) -> np.ndarray:
     """Fill tile (ti,tj)'s packed send buffer from the global tensor g.
     Regions without a neighbour are left as they were."""
     N, C, H, W = g.shape
     Ht, Wt = H // P, W // Q
-    offs, total = region_offsets(N, C, Ht, Wt, h)
+    offs, total = region_offsets(N, C, Ht, Wt, h, bw, send=True)
+    shapes = region_shapes(Ht, Wt, h, bw, send=True)
     assert send.shape == (total,)
     for d in DIRECTIONS:
-        rng = pack_region_ranges(H, W, P, Q, ti, tj, h, d)
+        rng = pack_region_ranges(H, W, P, Q, ti, tj, h, d, bw)
         if rng is None:
             continue
         (a0, a1), (b0, b1) = rng
         blk = g[:, :, a0:a1 + 1, b0:b1 + 1]
-        assert blk.shape[2:] == region_shapes(Ht, Wt, h)[d]
+        if 0 in shapes[d]:
+            continue
+        assert blk.shape[2:] == shapes[d]
         send[offs[d]:offs[d] + blk.size] = blk.reshape(-1)
     return send
 
 
-def halo_unpack(recv: np.ndarray, N, C, H, W, P, Q, ti, tj, h, window: np.ndarray) -> np.ndarray:
+def halo_unpack(recv: np.ndarray, N, C, H, W, P, Q, ti, tj, h, window: np.ndarray, bw=None) -> np.ndarray:
     """Write the halo part of tile (ti,tj)'s window [N,C,Ht+2h,Wt+2h].
 
     ``recv`` is the tile's packed receive buffer: its region d holds what the
-    neighbour in direction d sent (see ``gather_recv``).  Halo elements with
-    no neighbour are the domain's zero padding.  The owned block is untouched."""
+    neighbour in direction d sent (see ``gather_recv``).  The band of margin d
+    takes region d where the neighbour exists; every other margin cell (no
+    neighbour: the domain's zero padding; outside the bands: never read) is
+    zero.  The owned block is untouched."""
     Ht, Wt = H // P, W // Q
-    offs, _ = region_offsets(N, C, Ht, Wt, h)
+    a, b, l, r = _bands(h, bw)
+    offs, _ = region_offsets(N, C, Ht, Wt, h, bw)
+    window[:, :, :h, :] = 0
+    window[:, :, h + Ht:, :] = 0
+    window[:, :, :, :h] = 0
+    window[:, :, :, h + Wt:] = 0
     for d in DIRECTIONS:
         di, dj = STEP[d]
-        # margin d of the window, in window coordinates (inclusive)
-        rows = {-1: (0, h - 1), 0: (h, h + Ht - 1), 1: (h + Ht, Ht + 2 * h - 1)}[di]
-        cols = {-1: (0, h - 1), 0: (h, h + Wt - 1), 1: (h + Wt, Wt + 2 * h - 1)}[dj]
-        r, c = rows[1] - rows[0] + 1, cols[1] - cols[0] + 1
-        if neighbour(P, Q, ti, tj, d) is None:
-            window[:, :, rows[0]:rows[1] + 1, cols[0]:cols[1] + 1] = 0
+        # the band of margin d, in window coordinates (inclusive)
+        rows = {-1: (h - a, h - 1), 0: (h, h + Ht - 1), 1: (h + Ht, h + Ht + b - 1)}[di]
+        cols = {-1: (h - l, h - 1), 0: (h, h + Wt - 1), 1: (h + Wt, h + Wt + r - 1)}[dj]
+        nr, nc = rows[1] - rows[0] + 1, cols[1] - cols[0] + 1
+        if nr <= 0 or nc <= 0 or neighbour(P, Q, ti, tj, d) is None:
             continue
-        blk = recv[offs[d]:offs[d] + N * C * r * c].reshape(N, C, r, c)
+        blk = recv[offs[d]:offs[d] + N * C * nr * nc].reshape(N, C, nr, nc)
         window[:, :, rows[0]:rows[1] + 1, cols[0]:cols[1] + 1] = blk
     return window
 
 
-def gather_recv(sends: dict, N, C, H, W, P, Q, ti, tj, h) -> np.ndarray:
-    """Assemble tile (ti,tj)'s receive buffer: region d := neighbour d's
+def gather_recv(sends: dict, N, C, H, W, P, Q, ti, tj, h, bw=None) -> np.ndarray:
+    """Assemble tile (ti,tj)'s receive buffer: region d := neighbour d's send
     region OPPOSITE[d].  Regions without a neighbour are zero."""
     Ht, Wt = H // P, W // Q
-    offs, total = region_offsets(N, C, Ht, Wt, h)
-    shapes = region_shapes(Ht, Wt, h)
+    offs, total = region_offsets(N, C, Ht, Wt, h, bw)
+    soffs, _ = region_offsets(N, C, Ht, Wt, h, bw, send=True)
+    shapes = region_shapes(Ht, Wt, h, bw)
     recv = np.zeros(total, next(iter(sends.values())).dtype)
     for d in DIRECTIONS:
         nb = neighbour(P, Q, ti, tj, d)
@@ -306,7 +345,7 @@ def gather_recv(sends: dict, N, C, H, W, P, Q, ti, tj, h) -> np.ndarray:
             continue
         o = OPPOSITE[d]
         n = N * C * shapes[d][0] * shapes[d][1]
-        recv[offs[d]:offs[d] + n] = sends[nb][offs[o]:offs[o] + n]
+        recv[offs[d]:offs[d] + n] = sends[nb][soffs[o]:soffs[o] + n]
     return recv
 
 
@@ -341,11 +380,26 @@ def needed_halo_dy(Ho, R, stride, pad, Ht, Hot, t0_in, t0_out):
     return lo, hi
 
 
+def halo_bands(which, H, W, R, S, stride, pad, P, Q):
+    """Band widths (above, below, left, right) a tile's passes read beyond it:
+    x for Eq. (1)/(2), dy for Eq. (3), by brute force over the index sets of
+    the first tile (every tile of an aligned grid reads the same margins)."""
+    Ho, Wo = out_size(H, R, stride, pad), out_size(W, S, stride, pad)
+    Ht, Wt, Hot, Wot = H // P, W // Q, Ho // P, Wo // Q
+    if which == "x":
+        rows = needed_halo_x(H, R, stride, pad, Ho, Ht, Hot, 0, 0)
+        cols = needed_halo_x(W, S, stride, pad, Wo, Wt, Wot, 0, 0)
+    else:
+        rows = needed_halo_dy(Ho, R, stride, pad, Ht, Hot, 0, 0)
+        cols = needed_halo_dy(Wo, S, stride, pad, Wt, Wot, 0, 0)
+    return rows[0], rows[1], cols[0], cols[1]
+
+
 # --------------------------------------------------------------------------
 # Decomposed (tiled) computation, Sec. III-A
 # --------------------------------------------------------------------------
 
-def tiled_conv(x, w, dy, P, Q, h, pad, stride=1):
+def tiled_conv(x, w, dy, P, Q, h, pad, stride=1, bands=False):
     """Decomposed forward, backward-data and backward-filter over a P x Q grid
     of blocked tiles with halo width h >= needed (Sec. III-A).  With stride s
     an input tile of Ht x Wt owns the Ht/s x Wt/s output block whose taps start
@@ -356,7 +410,9 @@ def tiled_conv(x, w, dy, P, Q, h, pad, stride=1):
           above the tile, so the taps are shifted by h*s (pad + h*s);
       dw: Eq. (2) over the dy interior and the same x rows as y.
     y and dx are stitched; the dw partials are summed in fp64 in row-major
-    tile order.  Returns (y, dx, dw) in fp64."""
+    tile order.  With bands=True each window holds only the halo bands of
+    ``halo_bands`` (zeros in the rest of the margin).  Returns (y, dx, dw) in
+    fp64."""
     N, C, H, W = x.shape
     K, _, R, S = w.shape
     Ht, Wt = H // P, W // Q
@@ -367,8 +423,10 @@ def tiled_conv(x, w, dy, P, Q, h, pad, stride=1):
     dw = np.zeros((K, C, R, S))
     for ti in range(P):
         for tj in range(Q):
-            xw = tile_window(x, P, Q, ti, tj, h)
-            dyw = tile_window(dy, P, Q, ti, tj, h)    # dy tiles are Hot x Wot, same grid
+            bx = halo_bands("x", H, W, R, S, stride, pad, P, Q) if bands else None
+            by = halo_bands("dy", H, W, R, S, stride, pad, P, Q) if bands else None
+            xw = tile_window(x, P, Q, ti, tj, h, bx)
+            dyw = tile_window(dy, P, Q, ti, tj, h, by)    # dy tiles are Hot x Wot, same grid
             xs = np.ascontiguousarray(xw[:, :, h - pad:h - pad + nr, h - pad:h - pad + ns])
             yt = conv_fwd(xs, w, stride, 0)
             dxt = conv_bwd_data(np.ascontiguousarray(dyw), w, Ht, Wt, stride, pad + h * stride)

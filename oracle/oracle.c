@@ -189,3 +189,6 @@ void oracle_conv_bwd_filter_points(i64 N, i64 C, i64 K, i64 Hi, i64 Wi, i64 Ho, 
 
 /* Threads the OpenMP loops above use (for reporting timings). */
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+
+/* Run the loops above on n threads from now on (timing at one thread). */
+void oracle_set_num_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }

@@ -31,6 +31,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 DC_F32, DC_BF16 = 0, 1
 DC_X, DC_DY = 0, 1
 DC_ALL_TILES = -1
+DC_BAND_NS, DC_BAND_WE, DC_BAND_CORNERS, DC_BAND_ALL = 1, 2, 4, 7
 # capacity of the fixed workspace of dc_conv_bwd_filter_noalloc (include/dc.h)
 BWD_FILTER_NOALLOC_MAX_BYTES = 64 << 20
 
@@ -42,8 +43,9 @@ STATUS = {
 
 EXPORTS = (
     "dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_halo_pack", "dc_halo_unpack",
-    "dc_conv_bwd_filter_noalloc", "dc_validate", "dc_tile_pitch", "dc_tile_elems", "dc_halo_elems",
-    "dc_bwd_filter_workspace_bytes", "dc_required_halo", "dc_tile_dims", "dc_status_string",
+    "dc_conv_bwd_filter_noalloc", "dc_halo_pack_bands", "dc_halo_unpack_bands", "dc_validate",
+    "dc_tile_pitch", "dc_tile_elems", "dc_halo_elems", "dc_bwd_filter_workspace_bytes",
+    "dc_required_halo", "dc_halo_bands", "dc_tile_dims", "dc_status_string",
 )
 
 
@@ -78,6 +80,9 @@ _lib.dc_conv_bwd_filter.argtypes = [_P, _I, _V, _V, _V, _I, _V, ctypes.c_size_t,
 _lib.dc_conv_bwd_filter_noalloc.argtypes = [_P, _I, _V, _V, _V, _I, _V]
 _lib.dc_halo_pack.argtypes = [_P, _I, _I, _V, _V, _V]
 _lib.dc_halo_unpack.argtypes = [_P, _I, _I, _V, _V, _V]
+_lib.dc_halo_pack_bands.argtypes = [_P, _I, _I, _I, _V, _V, _V]
+_lib.dc_halo_unpack_bands.argtypes = [_P, _I, _I, _I, _V, _V, _V]
+_lib.dc_halo_bands.argtypes = [_P, _I, ctypes.POINTER(_I)]
 _lib.dc_validate.argtypes = [_P, _I]
 _lib.dc_tile_pitch.argtypes = [_P, _I]
 _lib.dc_tile_pitch.restype = ctypes.c_int64
@@ -92,8 +97,8 @@ _lib.dc_tile_dims.argtypes = [_P, ctypes.POINTER(_I)]
 _lib.dc_status_string.argtypes = [_I]
 _lib.dc_status_string.restype = ctypes.c_char_p
 for _n in ("dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_conv_bwd_filter_noalloc",
-           "dc_halo_pack",
-           "dc_halo_unpack", "dc_validate", "dc_required_halo", "dc_tile_dims"):
+           "dc_halo_pack", "dc_halo_unpack", "dc_halo_pack_bands", "dc_halo_unpack_bands",
+           "dc_validate", "dc_required_halo", "dc_halo_bands", "dc_tile_dims"):
     getattr(_lib, _n).restype = ctypes.c_int32
 
 
@@ -151,6 +156,13 @@ def required_halo(prob, which):
     return out[0], out[1]
 
 
+def halo_bands(prob, which):
+    """Band widths (above, below, left, right) the halo calls move for x or dy."""
+    out = (_I * 4)()
+    _check(_lib.dc_halo_bands(ctypes.byref(prob), which, out), "dc_halo_bands")
+    return tuple(out)
+
+
 def tile_dims(prob):
     out = (_I * 4)()
     _check(_lib.dc_tile_dims(ctypes.byref(prob), out), "dc_tile_dims")
@@ -204,3 +216,15 @@ def halo_unpack(prob, tile, which, recv, t_pad, stream=None):
     """Fill the margins of t_pad from the receive buffer (zeros at the domain edge)."""
     _check(_lib.dc_halo_unpack(ctypes.byref(prob), tile, which, _ptr(recv), _ptr(t_pad),
                                _stream(stream)), "dc_halo_unpack")
+
+
+def halo_pack_bands(prob, tile, which, bands, t_pad, send, stream=None):
+    """halo_pack restricted to the DC_BAND_* classes in `bands`."""
+    _check(_lib.dc_halo_pack_bands(ctypes.byref(prob), tile, which, bands, _ptr(t_pad), _ptr(send),
+                                   _stream(stream)), "dc_halo_pack_bands")
+
+
+def halo_unpack_bands(prob, tile, which, bands, recv, t_pad, stream=None):
+    """halo_unpack restricted to the DC_BAND_* classes in `bands`."""
+    _check(_lib.dc_halo_unpack_bands(ctypes.byref(prob), tile, which, bands, _ptr(recv), _ptr(t_pad),
+                                     _stream(stream)), "dc_halo_unpack_bands")

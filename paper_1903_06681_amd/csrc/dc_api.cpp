@@ -34,6 +34,13 @@ static void dy_margins(int t_in, int t_out, int R, int stride, int pad, int* lo,
     *hi = int(std::max<int64_t>(0, mmax - (t_out - 1)));
 }
 
+// Elements per plane of the eight bands of a ht x wt tile with band widths
+// bw = {above, below, left, right}.
+static int64_t halo_band_elems(const int bw[4], int ht, int wt) {
+    const int64_t rows = bw[0] + bw[1], cols = bw[2] + bw[3];
+    return rows * wt + int64_t(ht) * cols + rows * cols;
+}
+
 dc_status make_geo(const dc_problem* p, Geo* g) {
     if (!p || !g) return DC_ERR_NULL;
     std::memset(g, 0, sizeof(*g));
@@ -82,10 +89,15 @@ dc_status make_geo(const dc_problem* p, Geo* g) {
     g->dy_pitch = round_up(g->dy_cols, align);
     g->x_tile = int64_t(g->N) * g->C * g->x_rows * g->x_pitch;
     g->dy_tile = int64_t(g->N) * g->K * g->dy_rows * g->dy_pitch;
-    int64_t hx = 2 * int64_t(g->h) * (g->Ht + g->Wt) + 4 * int64_t(g->h) * g->h;
-    int64_t hy = 2 * int64_t(g->h) * (g->Hot + g->Wot) + 4 * int64_t(g->h) * g->h;
-    g->x_halo = int64_t(g->N) * g->C * hx;
-    g->dy_halo = int64_t(g->N) * g->K * hy;
+    // bands: the margins each pass reads (Sec. III-A), per side
+    const int bx[4] = {g->need_x_lo_r, g->need_x_hi_r, g->need_x_lo_s, g->need_x_hi_s};
+    const int by[4] = {g->need_dy_lo_r, g->need_dy_hi_r, g->need_dy_lo_s, g->need_dy_hi_s};
+    for (int i = 0; i < 4; ++i) { g->bw_x[i] = bx[i]; g->bw_dy[i] = by[i]; }
+    // packed buffers end on a 16-byte boundary, so that the consecutive
+    // per-tile buffers of an all-tiles call each start 16-byte aligned
+    auto round16 = [&](int64_t e) { const int64_t a = 16 / g->esize; return (e + a - 1) / a * a; };
+    g->x_halo = round16(int64_t(g->N) * g->C * halo_band_elems(g->bw_x, g->Ht, g->Wt));
+    g->dy_halo = round16(int64_t(g->N) * g->K * halo_band_elems(g->bw_dy, g->Hot, g->Wot));
     int64_t y_tile = int64_t(g->N) * g->K * g->Hot * g->Wot;
     int64_t dx_tile = int64_t(g->N) * g->C * g->Ht * g->Wt;
     int64_t w_elems = int64_t(g->K) * g->C * g->R * g->S;
@@ -131,16 +143,17 @@ static void clear_stale_error() { (void)hipGetLastError(); }
 
 // ---------------------------------------------------------------- halo
 
-static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which,
+static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which, int32_t bands,
                              const void* src, void* dst, bool unpack, void* stream) {
     Geo g;
     dc_status st = make_geo_tile(prob, tile, &g);
     if (st != DC_OK) return st;
     if (which != DC_X && which != DC_DY) return DC_ERR_ARG;
+    if (bands <= 0 || (bands & ~DC_BAND_ALL) != 0) return DC_ERR_ARG;
     const bool x = which == DC_X;
     const int ch = x ? g.C : g.K;
     const int Ht = x ? g.Ht : g.Hot, Wt = x ? g.Wt : g.Wot;
-    if (g.h == 0) return DC_OK;  // K = 1: no halo (Sec. III-A)
+    if (g.h == 0) return DC_OK;  // K = 1: no margin at all (Sec. III-A)
     if (!src || !dst) return DC_ERR_NULL;
     if (misaligned(src) || misaligned(dst)) return DC_ERR_ALIGN;
     HaloArgs a;
@@ -152,10 +165,39 @@ static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which
     a.rows = x ? g.x_rows : g.dy_rows;
     a.pitch = x ? g.x_pitch : g.dy_pitch;
     a.ht = Ht; a.wt = Wt; a.h = g.h;
+    const int* bw = x ? g.bw_x : g.bw_dy;
+    for (int i = 0; i < 4; ++i) a.bw[i] = bw[i];
+    // region offsets: receive region d has margin d's band shape, send region
+    // d the shape of margin opposite(d) (order N, S, W, E, NW, NE, SW, SE)
+    static const int di[8] = {-1, 1, 0, 0, -1, -1, 1, 1}, dj[8] = {0, 0, -1, 1, -1, 1, -1, 1};
+    auto band = [&](int d) {
+        const int64_t r = di[d] < 0 ? bw[0] : di[d] > 0 ? bw[1] : Ht;
+        const int64_t c = dj[d] < 0 ? bw[2] : dj[d] > 0 ? bw[3] : Wt;
+        return int64_t(a.planes) * r * c;
+    };
+    static const int opp[8] = {1, 0, 3, 2, 7, 6, 5, 4};
+    int64_t ro = 0, so = 0;
+    for (int d = 0; d < 8; ++d) {
+        a.roff[d] = ro; ro += band(d);
+        a.soff[d] = so; so += band(opp[d]);
+    }
     a.P = g.P; a.Q = g.Q;
     a.all_tiles = tile == DC_ALL_TILES;
     a.tile0 = a.all_tiles ? 0 : tile;
     a.ntiles = a.all_tiles ? g.ntiles : 1;
+    a.src_elems = unpack ? (a.all_tiles ? int64_t(g.ntiles) * a.halo_elems : a.halo_elems) : a.tile_elems;
+    a.bands = bands;
+    // N/S rows as aligned 16-byte vectors: rows of whole vectors that start on
+    // a 16-byte boundary in every buffer (tile rows are 16-byte aligned)
+    const int ve = 16 / g.esize;
+    a.vec = Wt % ve == 0 && a.halo_elems % ve == 0 && a.roff[1] % ve == 0 && a.soff[1] % ve == 0;
+    // Row bands and corners: a few hundred workgroups per launch, several
+    // planes each beyond that (thousands of tiny workgroups cost more to
+    // dispatch than they move).  With W/E columns one plane per workgroup:
+    // their gathers touch a cache line per element and go faster with more
+    // workgroups in flight (measured on a 4x4 grid of 256x256 tiles).
+    const int64_t planes_total = int64_t(a.planes) * a.ntiles;
+    a.ppw = (bands & DC_BAND_WE) ? 1 : int(std::max<int64_t>(1, std::min<int64_t>(16, planes_total / 512)));
     hipStream_t s = static_cast<hipStream_t>(stream);
     clear_stale_error();
     return launched(unpack ? launch_halo_unpack(a, g.esize, s) : launch_halo_pack(a, g.esize, s));
@@ -258,12 +300,32 @@ const char* dc_status_string(int32_t s) {
 
 dc_status dc_halo_pack(const dc_problem* prob, int32_t tile, int32_t which,
                        const void* t_pad, void* send, void* stream) {
-    return halo_common(prob, tile, which, t_pad, send, false, stream);
+    return halo_common(prob, tile, which, DC_BAND_ALL, t_pad, send, false, stream);
 }
 
 dc_status dc_halo_unpack(const dc_problem* prob, int32_t tile, int32_t which,
                          const void* recv, void* t_pad, void* stream) {
-    return halo_common(prob, tile, which, recv, t_pad, true, stream);
+    return halo_common(prob, tile, which, DC_BAND_ALL, recv, t_pad, true, stream);
+}
+
+dc_status dc_halo_pack_bands(const dc_problem* prob, int32_t tile, int32_t which, int32_t bands,
+                             const void* t_pad, void* send, void* stream) {
+    return halo_common(prob, tile, which, bands, t_pad, send, false, stream);
+}
+
+dc_status dc_halo_unpack_bands(const dc_problem* prob, int32_t tile, int32_t which, int32_t bands,
+                               const void* recv, void* t_pad, void* stream) {
+    return halo_common(prob, tile, which, bands, recv, t_pad, true, stream);
+}
+
+dc_status dc_halo_bands(const dc_problem* prob, int32_t which, int32_t bw[4]) {
+    if (!bw) return DC_ERR_NULL;
+    Geo g;
+    dc_status st = make_geo(prob, &g);
+    if (st != DC_OK) return st;
+    if (which != DC_X && which != DC_DY) return DC_ERR_ARG;
+    for (int i = 0; i < 4; ++i) bw[i] = which == DC_X ? g.bw_x[i] : g.bw_dy[i];
+    return DC_OK;
 }
 
 dc_status dc_conv_fwd(const dc_problem* prob, int32_t tile, const void* x_pad,

@@ -24,6 +24,8 @@ struct Geo {
     // margins the passes read beyond a tile, per spatial dimension
     int need_x_lo_r, need_x_hi_r, need_x_lo_s, need_x_hi_s;
     int need_dy_lo_r, need_dy_hi_r, need_dy_lo_s, need_dy_hi_s;
+    // halo bands moved by pack/unpack: rows above, below, cols left, right
+    int bw_x[4], bw_dy[4];
 };
 
 // Fill g from prob and check everything that does not depend on a tile index.

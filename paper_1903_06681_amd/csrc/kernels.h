@@ -7,25 +7,37 @@
 
 #include <cstdint>
 
+#include "dc.h"
+
 namespace dc {
 
 // ---------------------------------------------------------------- halo
 
 // Packed halo format: eight regions, order N, S, W, E, NW, NE, SW, SE, each
-// [planes][rows][cols] with rows = h (N/S/corners) or Ht, cols = h (W/E/corners)
-// or Wt, at offsets given by the prefix sums of those sizes.
+// [planes][rows][cols].  Region d of a receive buffer has the shape of margin
+// d's band (rows bw[0] above / bw[1] below or ht; cols bw[2] left / bw[3]
+// right or wt); region d of a send buffer the shape of the band the neighbour
+// in direction d receives (its margin opposite(d)).  Offsets roff / soff are
+// prefix sums of those sizes.
 struct HaloArgs {
     const void* src;     // pack: padded tiles; unpack: packed buffers
     void* dst;           // pack: packed buffers; unpack: padded tiles
     int64_t tile_elems;  // elements per padded tile
     int64_t halo_elems;  // elements per packed buffer
+    int64_t src_elems;   // elements readable from src (unpack: bounds of the vector reads)
+    int64_t roff[8];     // receive buffer region offsets
+    int64_t soff[8];     // send buffer region offsets
     int planes;          // N * channels
     int rows, pitch;     // padded tile rows and row pitch
     int ht, wt, h;       // tile extent and margin width
+    int bw[4];           // band widths: rows above, rows below, cols left, cols right
     int P, Q;
     int tile0;           // first tile handled by this launch
     int ntiles;          // tiles handled by this launch
     int all_tiles;       // unpack: read neighbours' send buffers directly
+    int bands;           // DC_BAND_* classes moved by this launch
+    int vec;             // N/S rows may move as aligned 16-byte vectors
+    int ppw;             // planes per workgroup
 };
 
 hipError_t launch_halo_pack(const HaloArgs& a, int esize, hipStream_t s);

@@ -10,9 +10,10 @@ The paper estimates a convolutional layer's time under a distribution from
 
 with lower-case shapes local to one GPU.  A halo exchange with margin width
 O sends two north/south messages of O*n*ch*w elements, two east/west ones of
-O*n*ch*h and four corners of O^2*n*ch; the east/west and corner messages
-vanish when the width is not split, the north/south and corner ones when the
-height is not split.  Point-to-point messages follow the linear model
+O*n*ch*h and four corners of O^2*n*ch (with stride > 1 each side carries
+the band its receiver reads, which may be narrower); the east/west and corner
+messages vanish when the width is not split, the north/south and corner ones
+when the height is not split.  Point-to-point messages follow the linear model
 SR(m) = alpha + beta*m (full duplex, no interference, Sec. II-B); allreduces
 follow the collective models the paper cites (ring / recursive doubling).
 
@@ -119,22 +120,47 @@ def local_dims(layer: LayerShape, d: Distribution) -> Tuple[int, int, int, int, 
     return n, h, w, h // layer.stride, w // layer.stride
 
 
+def halo_bands(layer: LayerShape, d: Distribution, which: str) -> Tuple[int, int, int, int]:
+    """Band widths (above, below, left, right) of a tile's x halo ('x': the
+    rows and columns Eq. (1) reads beyond the tile) or dL/dy halo ('dy':
+    Eq. (3)).  At stride 1 with 'same' padding all four are O = layer.halo's
+    usual value; at stride > 1 one side may need fewer (Sec. III-A)."""
+    _, h, w, ho, wo = local_dims(layer, d)
+
+    def x_side(t_in, t_out, R):
+        return layer.pad, max(0, (t_out - 1) * layer.stride - layer.pad + R - 1 - (t_in - 1))
+
+    def dy_side(t_in, t_out, R):
+        st = layer.stride
+        mmin = -((R - 1 - layer.pad) // st)          # ceil((pad - (R-1)) / stride)
+        mmax = (t_in - 1 + layer.pad) // st
+        return max(0, -mmin), max(0, mmax - (t_out - 1))
+
+    side = x_side if which == "x" else dy_side
+    a, b = side(h, ho, layer.R)
+    l, r = side(w, wo, layer.S)
+    return a, b, l, r
+
+
 def halo_messages(layer: LayerShape, d: Distribution, which: str) -> List[Tuple[str, int]]:
     """Messages one interior GPU sends for the x halo ('x', forward) or the
     dL/dy halo ('dy', backward-data): (direction, elements), following the
-    region list of Sec. V-A with margin width O = layer.halo."""
+    region list of Sec. V-A.  A message toward direction d carries the band
+    the neighbour there reads on its opposite side (margin width O on every
+    side for the stride-1 layers of the paper)."""
     n, h, w, ho, wo = local_dims(layer, d)
-    O = layer.halo
-    if O == 0 or (d.P == 1 and d.Q == 1):
+    if layer.halo == 0 or (d.P == 1 and d.Q == 1):
         return []
     ch, th, tw = (layer.C, h, w) if which == "x" else (layer.F, ho, wo)
+    bn, bs, bw, be = halo_bands(layer, d, which)
     msgs = []
     if d.P > 1:
-        msgs += [("N", O * n * ch * tw), ("S", O * n * ch * tw)]
+        msgs += [("N", bs * n * ch * tw), ("S", bn * n * ch * tw)]
     if d.Q > 1:
-        msgs += [("W", O * n * ch * th), ("E", O * n * ch * th)]
+        msgs += [("W", be * n * ch * th), ("E", bw * n * ch * th)]
     if d.P > 1 and d.Q > 1:
-        msgs += [(c, O * O * n * ch) for c in ("NW", "NE", "SW", "SE")]
+        msgs += [("NW", bs * be * n * ch), ("NE", bs * bw * n * ch),
+                 ("SW", bn * be * n * ch), ("SE", bn * bw * n * ch)]
     return msgs
 
 

@@ -38,7 +38,7 @@ def _bits(t):
     return t.view(torch.int16 if t.element_size() == 2 else torch.int32)
 
 
-@pytest.mark.parametrize("name", ["c5a", "c4", "c5b"])
+@pytest.mark.parametrize("name", ["c5a", "c4", "c5b", "c3a_2x2", "c4s2"])
 @pytest.mark.parametrize("which", [X, DY])
 def test_halo_full_size_all_tiles_bit_exact(name, which):
     L = wl.LAYERS[name]
@@ -48,6 +48,7 @@ def test_halo_full_size_all_tiles_bit_exact(name, which):
     g = wl.draw(L, "x" if which == X else "dy")
     tw = L.Wt if which == X else L.Wot
     h = L.halo
+    bw = orc.halo_bands("x" if which == X else "dy", L.H, L.W, L.R, L.S, L.stride, L.pad, L.P, L.Q)
     tiles = H.alloc_tiles(p, which, nt, L.dtype)
     H.scatter_interiors(tiles, H.to_device(g, L.dtype), p, which)
     hel = dc.halo_elems(p, which)
@@ -59,11 +60,12 @@ def test_halo_full_size_all_tiles_bit_exact(name, which):
     for t in range(nt):
         ti, tj = divmod(t, L.Q)
         ref = np.full(hel, sentinel, np.float32)
-        orc.halo_pack(g, L.P, L.Q, ti, tj, h, ref)
+        ntot = orc.region_offsets(L.N, L.C if which == X else L.K, *((L.Ht, L.Wt) if which == X else (L.Hot, L.Wot)), h, bw)[1]
+        orc.halo_pack(g, L.P, L.Q, ti, tj, h, ref[:ntot], bw)   # padding to 16 bytes stays untouched
         rb = _bits(H.to_device(ref, L.dtype))
         bad = int((_bits(send[t]) != rb).sum())
         assert bad == 0, f"pack tile {t}: {bad} mismatches"
-        win = H.to_device(orc.tile_window(g, L.P, L.Q, ti, tj, h), L.dtype)
+        win = H.to_device(orc.tile_window(g, L.P, L.Q, ti, tj, h, bw), L.dtype)
         got = tiles[t][:, :, :, :tw + 2 * h].contiguous()
         bad = int((_bits(got) != _bits(win)).sum())
         assert bad == 0, f"unpack tile {t}: {bad} mismatches"

@@ -237,9 +237,16 @@ def _bits(t):
     return t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).cpu().numpy()
 
 
-@pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5b_s", "c4_s"])
+def _oracle_bands(L, which):
+    return orc.halo_bands("x" if which == X else "dy", L.H, L.W, L.R, L.S, L.stride, L.pad, L.P, L.Q)
+
+
+@pytest.mark.parametrize("name", ["c2", "odd_f32", "odd_bf16", "c5b_s", "c4_s", "s2dec_bf16",
+                                  "s2k7dec_f32", "bp7_bf16", "s2taps_bf16", "wide_bf16"])
 @pytest.mark.parametrize("which", [X, DY])
 def test_halo_pack_unpack_bit_exact(name, which):
+    """Bands per side (one-sided at stride 2, narrower than the margin for
+    odd_*), margins beyond the bands zeroed, pitch columns never written."""
     L = SMALL[name]
     p = dc.Problem.of(L)
     nt = L.P * L.Q
@@ -257,23 +264,75 @@ def test_halo_pack_unpack_bit_exact(name, which):
     torch.cuda.synchronize()
     sb, tb = _bits(send), _bits(tiles)
     h = L.halo
+    bw = _oracle_bands(L, which)
     gq = g if L.dtype == "f32" else g  # values already bf16-representable
     for t in range(nt):
         ti, tj = divmod(t, L.Q)
         # pack: regions with a neighbour equal the oracle's; the rest untouched (NaN)
         ref = np.full(hel, sentinel, np.float32)
-        orc.halo_pack(gq, L.P, L.Q, ti, tj, h, ref)
+        ntot = orc.region_offsets(L.N, L.C if which == X else L.K, *((L.Ht, L.Wt) if which == X else (L.Hot, L.Wot)), h, bw)[1]
+        orc.halo_pack(gq, L.P, L.Q, ti, tj, h, ref[:ntot], bw)   # padding to 16 bytes stays untouched
         rb = _bits(H.to_device(ref, L.dtype))
         bad = np.nonzero(sb[t] != rb)[0]
         assert bad.size == 0, f"pack tile {t}: {bad.size} mismatches, first at {bad[:5]}: {sb[t][bad[:5]]} vs {rb[bad[:5]]}"
         # unpack: the window equals the zero-padded global slice; pitch columns untouched
-        win = orc.tile_window(gq, L.P, L.Q, ti, tj, h)
+        win = orc.tile_window(gq, L.P, L.Q, ti, tj, h, bw)
         wb = _bits(H.to_device(win, L.dtype))
         got = tb[t][:, :, :, :tw + 2 * h]
         bad = np.argwhere(got != wb)
         assert bad.size == 0, f"unpack tile {t}: {len(bad)} mismatches, first {bad[:5].tolist()}"
         pad_cols = tiles[t][:, :, :, tw + 2 * h:]
         assert bool(torch.isnan(pad_cols.float()).all()), "pitch padding written"
+
+
+@pytest.mark.parametrize("name", ["c5b_s", "odd_bf16", "s2dec_bf16", "c4_s"])
+@pytest.mark.parametrize("which", [X, DY])
+def test_halo_band_classes_compose_to_the_full_calls(name, which):
+    """Pack and unpack by band class (N/S rows, W/E columns, corners), one
+    class per call, give the full calls' bits; each class writes only its
+    own regions (pack) and its own margin cells (unpack)."""
+    L = SMALL[name]
+    p = dc.Problem.of(L)
+    nt = L.P * L.Q
+    g = wl.draw(L, "x" if which == X else "dy")
+    tiles = H.alloc_tiles(p, which, nt, L.dtype)
+    H.scatter_interiors(tiles, H.to_device(g, L.dtype), p, which)
+    hel = dc.halo_elems(p, which)
+    tdt = H.TORCH_DT[L.dtype]
+    full = torch.full((nt, hel), -3.0, dtype=tdt, device="cuda")
+    parts = torch.full((nt, hel), -3.0, dtype=tdt, device="cuda")
+    dc.halo_pack(p, ALL, which, tiles, full)
+    table = H.region_table(p, which, send=True)
+    cls = {dc.DC_BAND_NS: ("N", "S"), dc.DC_BAND_WE: ("W", "E"),
+           dc.DC_BAND_CORNERS: ("NW", "NE", "SW", "SE")}
+    ch = L.C if which == X else L.K
+    for band, dirs in cls.items():
+        before = parts.clone()
+        dc.halo_pack_bands(p, ALL, which, band, tiles, parts)
+        torch.cuda.synchronize()
+        changed = (_bits(parts) != _bits(before))
+        for d, (off, r, c) in table.items():
+            if d not in dirs:
+                assert not changed[:, off:off + L.N * ch * r * c].any(), (band, d)
+    assert np.array_equal(_bits(parts), _bits(full))
+    # unpack: the full call vs one class at a time, both into NaN margins
+    t_full = tiles.clone()
+    t_parts = tiles.clone()
+    dc.halo_unpack(p, ALL, which, full, t_full)
+    h = L.halo
+    th, tw = (L.Ht, L.Wt) if which == X else (L.Hot, L.Wot)
+    rows = np.arange(th + 2 * h)[:, None]
+    cols = np.arange(tw + 2 * h)[None, :]
+    rin, cin = (rows >= h) & (rows < h + th), (cols >= h) & (cols < h + tw)
+    cells = {dc.DC_BAND_NS: ~rin & cin, dc.DC_BAND_WE: rin & ~cin, dc.DC_BAND_CORNERS: ~rin & ~cin}
+    for band, mask in cells.items():
+        before = _bits(t_parts).copy()
+        dc.halo_unpack_bands(p, ALL, which, band, full, t_parts)
+        torch.cuda.synchronize()
+        after = _bits(t_parts)
+        diff = (after != before)[..., :tw + 2 * h].any(axis=(0, 1, 2))
+        assert not (diff & ~mask).any(), band
+    assert np.array_equal(_bits(t_parts), _bits(t_full))
 
 
 def test_unpack_writes_only_margins():

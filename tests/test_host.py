@@ -106,12 +106,36 @@ def test_one_by_one_needs_no_halo_and_packs_nothing():
     dc.halo_unpack(p, dc.DC_ALL_TILES, dc.DC_X, A16, A32, 0)
 
 
+@pytest.mark.parametrize("R,S,stride,pad,H,W,P,Q", [
+    (3, 3, 1, 1, 32, 32, 2, 2), (5, 5, 1, 2, 40, 40, 4, 4), (1, 1, 1, 0, 16, 16, 2, 2),
+    (7, 7, 2, 3, 224, 224, 2, 2), (3, 3, 2, 1, 32, 32, 2, 2), (7, 7, 2, 3, 64, 64, 4, 4),
+    (3, 5, 1, 1, 24, 40, 1, 1), (5, 3, 2, 2, 24, 36, 1, 1), (7, 7, 2, 3, 224, 224, 1, 1),
+    (5, 5, 2, 2, 24, 36, 3, 3),
+])
+def test_halo_bands_match_brute_force(R, S, stride, pad, H, W, P, Q):
+    """Bands per side (above, below, left, right) equal the oracle's brute
+    force over the index sets of Eqs. (1) and (3); halo_elems is the size of
+    the eight regions they span."""
+    p = prob(R=R, S=S, stride=stride, pad=pad, H=H, W=W, P=P, Q=Q, halo=max(R, S, 3) if P * Q == 1 else 3)
+    if dc.validate(p, 0) != 0:
+        p = prob(R=R, S=S, stride=stride, pad=pad, H=H, W=W, P=P, Q=Q, halo=max(R, S))
+    assert dc.validate(p, 0) == 0
+    Ht, Wt, Hot, Wot = dc.tile_dims(p)
+    for which, name, ch, th, tw in ((dc.DC_X, "x", p.C, Ht, Wt), (dc.DC_DY, "dy", p.K, Hot, Wot)):
+        bw = orc.halo_bands(name, H, W, R, S, stride, pad, P, Q)
+        assert dc.halo_bands(p, which) == bw, name
+        _, total = orc.region_offsets(p.N, ch, th, tw, p.halo, bw)
+        assert dc.halo_elems(p, which) == -(-total // 4) * 4   # fp32: 16-byte multiple
+
+
 def test_halo_elems_and_pitch_match_oracle_layout():
     for L in wl.LAYERS.values():
         p = dc.Problem.of(L)
-        for which, ch, th, tw in ((dc.DC_X, L.C, L.Ht, L.Wt), (dc.DC_DY, L.K, L.Hot, L.Wot)):
-            _, total = orc.region_offsets(L.N, ch, th, tw, L.halo)
-            assert dc.halo_elems(p, which) == total
+        for which, name, ch, th, tw in ((dc.DC_X, "x", L.C, L.Ht, L.Wt), (dc.DC_DY, "dy", L.K, L.Hot, L.Wot)):
+            bw = orc.halo_bands(name, L.H, L.W, L.R, L.S, L.stride, L.pad, L.P, L.Q)
+            _, total = orc.region_offsets(L.N, ch, th, tw, L.halo, bw)
+            al = 8 if L.dtype == "bf16" else 4
+            assert dc.halo_elems(p, which) == -(-total // al) * al
             pitch = dc.tile_pitch(p, which)
             esize = 2 if L.dtype == "bf16" else 4
             assert pitch >= tw + 2 * L.halo and (pitch * esize) % 16 == 0
@@ -136,6 +160,8 @@ def test_calls_reject_bad_arguments_before_launch():
     assert _status(dc.halo_pack, p, 0, 2, A16, A32, 0) == -10
     assert _status(dc.halo_unpack, p, 0, dc.DC_X, None, A32, 0) == -1
     assert _status(dc.halo_unpack, p, 0, dc.DC_DY, A16, MIS, 0) == -7
+    assert _status(dc.halo_pack_bands, p, 0, dc.DC_X, 0, A16, A32, 0) == -10
+    assert _status(dc.halo_unpack_bands, p, 0, dc.DC_X, 8, A16, A32, 0) == -10
 
 
 class _FakeWs:

@@ -226,6 +226,91 @@ def test_halo_round_trip_reproduces_padded_window(P, Q, h):
             assert np.array_equal(orc.tile_window(g, P, Q, ti, tj, h), brute)
 
 
+def _brute_band_window(g, P, Q, ti, tj, h, bw):
+    """The padded window with zeros outside the bands (above, below, left, right)."""
+    out = _brute_window(g, P, Q, ti, tj, h)
+    N, C, H, W = g.shape
+    Ht, Wt = H // P, W // Q
+    a, b, l, r = bw
+    for i in range(Ht + 2 * h):
+        for j in range(Wt + 2 * h):
+            if not (h - a <= i < h + Ht + b and h - l <= j < h + Wt + r):
+                out[:, :, i, j] = 0
+    return out
+
+
+@pytest.mark.parametrize("P,Q,h,bw", [(2, 2, 3, (3, 2, 3, 2)), (3, 2, 2, (0, 1, 1, 0)),
+                                      (2, 3, 2, (1, 2, 2, 1)), (4, 4, 1, (1, 0, 0, 1)),
+                                      (2, 2, 2, (2, 2, 2, 2)), (1, 1, 2, (1, 1, 2, 0))])
+def test_halo_round_trip_with_per_side_bands(P, Q, h, bw):
+    """With band widths (above, below, left, right) narrower than the margin,
+    pack -> exchange -> unpack fills each margin band from the neighbour,
+    zeros the rest of the margin, and leaves the owned block alone; the send
+    and receive buffers hold the same number of elements."""
+    rng = np.random.default_rng(P * 10 + Q + h + sum(bw))
+    N, C, H, W = 2, 3, 6 * P, 6 * Q
+    g = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    Ht, Wt = H // P, W // Q
+    _, total = orc.region_offsets(N, C, Ht, Wt, h, bw)
+    _, stotal = orc.region_offsets(N, C, Ht, Wt, h, bw, send=True)
+    assert total == stotal
+    sends = {(ti, tj): orc.halo_pack(g, P, Q, ti, tj, h, np.full(total, np.nan, np.float32), bw)
+             for ti in range(P) for tj in range(Q)}
+    for ti in range(P):
+        for tj in range(Q):
+            win = np.full((N, C, Ht + 2 * h, Wt + 2 * h), np.nan, np.float32)
+            win[:, :, h:h + Ht, h:h + Wt] = g[:, :, ti * Ht:(ti + 1) * Ht, tj * Wt:(tj + 1) * Wt]
+            recv = orc.gather_recv(sends, N, C, H, W, P, Q, ti, tj, h, bw)
+            orc.halo_unpack(recv, N, C, H, W, P, Q, ti, tj, h, win, bw)
+            brute = _brute_band_window(g, P, Q, ti, tj, h, bw)
+            assert np.array_equal(win, brute)
+            assert np.array_equal(orc.tile_window(g, P, Q, ti, tj, h, bw), brute)
+
+
+@pytest.mark.parametrize("R,stride,pad,x_bw,dy_bw", [
+    (3, 1, 1, (1, 1, 1, 1), (1, 1, 1, 1)),
+    (5, 1, 2, (2, 2, 2, 2), (2, 2, 2, 2)),
+    (1, 1, 0, (0, 0, 0, 0), (0, 0, 0, 0)),
+    (7, 2, 3, (3, 2, 3, 2), (1, 2, 1, 2)),   # ResNet conv1 on a grid
+    (3, 2, 1, (1, 0, 1, 0), (0, 1, 0, 1)),   # stride-2 block entry: one-sided halos
+])
+def test_halo_bands_closed_forms(R, stride, pad, x_bw, dy_bw):
+    """The bands the brute-force index sets give: x above = pad, below =
+    max(0, R - pad - stride); dy above = floor((R-1-pad)/stride), below =
+    floor((pad-1)/stride) + 1 (Sec. III-A: at stride > 1 a side may need no
+    halo)."""
+    H = W = 16 * stride
+    assert orc.halo_bands("x", H, W, R, R, stride, pad, 4, 4) == x_bw
+    assert orc.halo_bands("dy", H, W, R, R, stride, pad, 4, 4) == dy_bw
+    assert x_bw[:2] == (pad, max(0, R - pad - stride))
+    assert dy_bw[:2] == ((R - 1 - pad) // stride, (pad - 1) // stride + 1)
+
+
+@pytest.mark.parametrize("P,Q,h,R,pad,stride,kind", [
+    (2, 2, 3, 7, 3, 2, "int"), (4, 2, 3, 7, 3, 2, "real"), (2, 2, 1, 3, 1, 2, "int"),
+    (2, 3, 2, 3, 1, 1, "int"), (2, 2, 2, 5, 2, 1, "real"),
+])
+def test_decomposed_with_bands_only_equals_undecomposed(P, Q, h, R, pad, stride, kind):
+    """Windows that hold only the halo bands (zeros in the rest of the
+    margin) still give the undecomposed result: the bands are all the passes
+    read (y and dx bit for bit, dw bit for bit on integers)."""
+    rng = np.random.default_rng(P * 100 + Q * 10 + h + R + stride)
+    N, C, K = 2, 3, 4
+    H, W = 4 * stride * P, 3 * stride * Q
+    x = _rand(rng, (N, C, H, W), kind)
+    w = _rand(rng, (K, C, R, R), kind)
+    dy = _rand(rng, (N, K, H // stride, W // stride), kind)
+    y0 = orc.round_f32(orc.conv_fwd(x, w, stride, pad))
+    dx0 = orc.round_f32(orc.conv_bwd_data(dy, w, H, W, stride, pad))
+    dw0 = orc.round_f32(orc.conv_bwd_filter(x, dy, R, R, stride, pad))
+    y1, dx1, dw1 = (orc.round_f32(a) for a in orc.tiled_conv(x, w, dy, P, Q, h, pad, stride, bands=True))
+    assert np.array_equal(y0, y1) and np.array_equal(dx0, dx1)
+    if kind == "int":
+        assert np.array_equal(dw0, dw1)
+    else:
+        assert np.all(np.abs(dw0.astype(np.float64) - dw1) <= np.abs(np.spacing(dw0)))
+
+
 def test_halo_size_matches_message_terms():
     """An interior tile's halo holds 2*O*I_H + 2*O*I_W + 4*O^2 elements per
     (sample, channel): the east/west, north/south and corner terms of the
