@@ -216,6 +216,28 @@ dc_status dc_halo_pack_bands(const dc_problem* prob, int32_t tile, int32_t which
 dc_status dc_halo_unpack_bands(const dc_problem* prob, int32_t tile, int32_t which, int32_t bands,
                                const void* recv, void* t_pad, void* stream);
 
+/*
+ * Interior / boundary split of the forward and input-gradient passes, so that
+ * the halo exchange can overlap computation (Sec. IV-A; stride 1 only, else
+ * DC_ERR_UNSUPPORTED).  The boundary of the output tile is the frame of
+ * outputs whose sum reads a margin: for dc_conv_fwd_region the rows above /
+ * below and columns left / right of widths dc_halo_bands(DC_X); for
+ * dc_conv_bwd_data_region those of dc_halo_bands(DC_DY).
+ *   DC_REGION_ALL:      the plain call.
+ *   DC_REGION_INTERIOR: every output outside the frame is final; the frame is
+ *                       left unspecified.  It may run while the margins are
+ *                       being written (e.g. by dc_halo_unpack on another
+ *                       stream): margin values reach frame outputs only.
+ *   DC_REGION_BOUNDARY: computes the frame only (the margins must be in
+ *                       place); every other output is left untouched.
+ * INTERIOR followed by BOUNDARY gives the plain call's result.
+ */
+typedef enum { DC_REGION_ALL = 0, DC_REGION_INTERIOR = 1, DC_REGION_BOUNDARY = 2 } dc_region;
+dc_status dc_conv_fwd_region(const dc_problem* prob, int32_t tile, int32_t region, const void* x_pad,
+                             const void* w, float* y, void* stream);
+dc_status dc_conv_bwd_data_region(const dc_problem* prob, int32_t tile, int32_t region,
+                                  const void* dy_pad, const void* w, float* dx, void* stream);
+
 /* ---- host-only helpers (no GPU needed) ---- */
 
 /* Check a problem and tile index (DC_ALL_TILES allowed); no launch. */

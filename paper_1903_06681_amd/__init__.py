@@ -32,6 +32,7 @@ DC_F32, DC_BF16 = 0, 1
 DC_X, DC_DY = 0, 1
 DC_ALL_TILES = -1
 DC_BAND_NS, DC_BAND_WE, DC_BAND_CORNERS, DC_BAND_ALL = 1, 2, 4, 7
+DC_REGION_ALL, DC_REGION_INTERIOR, DC_REGION_BOUNDARY = 0, 1, 2
 # capacity of the fixed workspace of dc_conv_bwd_filter_noalloc (include/dc.h)
 BWD_FILTER_NOALLOC_MAX_BYTES = 64 << 20
 
@@ -43,7 +44,8 @@ STATUS = {
 
 EXPORTS = (
     "dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_halo_pack", "dc_halo_unpack",
-    "dc_conv_bwd_filter_noalloc", "dc_halo_pack_bands", "dc_halo_unpack_bands", "dc_validate",
+    "dc_conv_bwd_filter_noalloc", "dc_halo_pack_bands", "dc_halo_unpack_bands",
+    "dc_conv_fwd_region", "dc_conv_bwd_data_region", "dc_validate",
     "dc_tile_pitch", "dc_tile_elems", "dc_halo_elems", "dc_bwd_filter_workspace_bytes",
     "dc_required_halo", "dc_halo_bands", "dc_tile_dims", "dc_status_string",
 )
@@ -80,6 +82,8 @@ _lib.dc_conv_bwd_filter.argtypes = [_P, _I, _V, _V, _V, _I, _V, ctypes.c_size_t,
 _lib.dc_conv_bwd_filter_noalloc.argtypes = [_P, _I, _V, _V, _V, _I, _V]
 _lib.dc_halo_pack.argtypes = [_P, _I, _I, _V, _V, _V]
 _lib.dc_halo_unpack.argtypes = [_P, _I, _I, _V, _V, _V]
+_lib.dc_conv_fwd_region.argtypes = [_P, _I, _I, _V, _V, _V, _V]
+_lib.dc_conv_bwd_data_region.argtypes = [_P, _I, _I, _V, _V, _V, _V]
 _lib.dc_halo_pack_bands.argtypes = [_P, _I, _I, _I, _V, _V, _V]
 _lib.dc_halo_unpack_bands.argtypes = [_P, _I, _I, _I, _V, _V, _V]
 _lib.dc_halo_bands.argtypes = [_P, _I, ctypes.POINTER(_I)]
@@ -98,6 +102,7 @@ _lib.dc_status_string.argtypes = [_I]
 _lib.dc_status_string.restype = ctypes.c_char_p
 for _n in ("dc_conv_fwd", "dc_conv_bwd_data", "dc_conv_bwd_filter", "dc_conv_bwd_filter_noalloc",
            "dc_halo_pack", "dc_halo_unpack", "dc_halo_pack_bands", "dc_halo_unpack_bands",
+           "dc_conv_fwd_region", "dc_conv_bwd_data_region",
            "dc_validate", "dc_required_halo", "dc_halo_bands", "dc_tile_dims"):
     getattr(_lib, _n).restype = ctypes.c_int32
 
@@ -228,3 +233,15 @@ def halo_unpack_bands(prob, tile, which, bands, recv, t_pad, stream=None):
     """halo_unpack restricted to the DC_BAND_* classes in `bands`."""
     _check(_lib.dc_halo_unpack_bands(ctypes.byref(prob), tile, which, bands, _ptr(recv), _ptr(t_pad),
                                      _stream(stream)), "dc_halo_unpack_bands")
+
+
+def conv_fwd_region(prob, tile, region, x_pad, w, y, stream=None):
+    """Eq. (1) on the interior (no halo read) or the boundary frame of a tile."""
+    _check(_lib.dc_conv_fwd_region(ctypes.byref(prob), tile, region, _ptr(x_pad), _ptr(w), _ptr(y),
+                                   _stream(stream)), "dc_conv_fwd_region")
+
+
+def conv_bwd_data_region(prob, tile, region, dy_pad, w, dx, stream=None):
+    """Eq. (3) on the interior (no halo read) or the boundary frame of a tile."""
+    _check(_lib.dc_conv_bwd_data_region(ctypes.byref(prob), tile, region, _ptr(dy_pad), _ptr(w),
+                                        _ptr(dx), _stream(stream)), "dc_conv_bwd_data_region")

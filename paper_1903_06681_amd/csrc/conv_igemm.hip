@@ -47,6 +47,31 @@ __host__ __device__ inline int f32_plane_stride(int PR, int PC) {
 }
 
 
+// Output block of this workgroup: kBH rows x kBW columns from (u0, v0), with
+// stores limited to rows < uend and columns < vend.  Whole tile: blocks in
+// row-major order over Uo x Vo.  Frame mode: blocks of the segments in turn,
+// each a rectangle of the output (the boundary band of a tile).
+__device__ __forceinline__ void block_origin(const IgemmArgs& a, int& u0, int& v0, int& uend, int& vend) {
+    if (a.frame) {
+        int sg = 0;
+        while (sg + 1 < a.fseg && int(blockIdx.x) >= a.fblk[sg + 1]) ++sg;
+        const int local = blockIdx.x - a.fblk[sg];
+        const int nvb = (a.fnv[sg] + kBW - 1) / kBW;
+        const int vb = local % nvb, ub = local / nvb;
+        u0 = a.fu0[sg] + ub * kBH;
+        v0 = a.fv0[sg] + vb * kBW;
+        uend = a.fu0[sg] + a.fnu[sg];
+        vend = a.fv0[sg] + a.fnv[sg];
+    } else {
+        const int nvb = (a.Vo + kBW - 1) / kBW;
+        const int vb = blockIdx.x % nvb, ub = blockIdx.x / nvb;
+        u0 = ub * kBH;
+        v0 = vb * kBW;
+        uend = a.Uo;
+        vend = a.Vo;
+    }
+}
+
 template <int OB>
 __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -60,11 +85,10 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
     uint16_t* wl = reinterpret_cast<uint16_t*>(smem);   // [G][OB][8]
     uint16_t* pl = wl + G * OB * 8;                      // [PR][PC][PS]
 
-    const int nvb = (a.Vo + kBW - 1) / kBW;
-    const int vb = blockIdx.x % nvb, ub = blockIdx.x / nvb;
+    int u0, v0, uend, vend;
+    block_origin(a, u0, v0, uend, vend);
     const int o0 = blockIdx.y * OB;
     const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
-    const int u0 = ub * kBH, v0 = vb * kBW;
 
     const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
     const uint16_t* in = static_cast<const uint16_t*>(a.in) + tile * a.in_tile +
@@ -157,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
     // D layout of a 32x32 MFMA tile: value i of lane l is row 8*(i/4) + 4*(l/32) + i%4,
     // column l%32.  Rows are output channels, columns pixels.
     const int u = u0 + wave;
-    if (u >= a.Uo) return;
+    if (u >= uend) return;
     float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
     const int orow = u * a.ostr + a.oph_r;
 #pragma unroll
@@ -165,7 +189,7 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
             const int v = v0 + pb * 32 + l32;
-            if (v >= a.Vo) continue;
+            if (v >= vend) continue;
             const int ocol = v * a.ostr + a.oph_c;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -189,11 +213,10 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
     float* wl = reinterpret_cast<float*>(smem);   // [KG][OB]
     float* pl = wl + KG * OB;                     // [CC][PLN] with rows of PC
 
-    const int nvb = (a.Vo + kBW - 1) / kBW;
-    const int vb = blockIdx.x % nvb, ub = blockIdx.x / nvb;
+    int u0, v0, uend, vend;
+    block_origin(a, u0, v0, uend, vend);
     const int o0 = blockIdx.y * OB;
     const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
-    const int u0 = ub * kBH, v0 = vb * kBW;
 
     const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
     const float* in = static_cast<const float*>(a.in) + tile * a.in_tile +
@@ -259,7 +282,7 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
     }
 
     const int u = u0 + wave;
-    if (u >= a.Uo) return;
+    if (u >= uend) return;
     float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
     const int orow = u * a.ostr + a.oph_r;
 #pragma unroll
@@ -267,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
             const int v = v0 + pb * 32 + l32;
-            if (v >= a.Vo) continue;
+            if (v >= vend) continue;
             const int ocol = v * a.ostr + a.oph_c;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -289,13 +312,36 @@ static int lds_bytes_for(const IgemmArgs& a, int dtype, int CC, int OB) {
     return (Tt * CC * OB + CC * f32_plane_stride(PR, PC)) * 4;
 }
 
+void igemm_set_frame(IgemmArgs& a, const int bands[4]) {
+    a.frame = 1;
+    a.fseg = 0;
+    const int top = std::min(bands[0], a.Uo), bot = std::min(bands[1], a.Uo - top);
+    const int mid = a.Uo - top - bot;
+    const int left = std::min(bands[2], a.Vo), right = std::min(bands[3], a.Vo - left);
+    auto add = [&](int u0, int nu, int v0, int nv) {
+        if (nu <= 0 || nv <= 0) return;
+        const int k = a.fseg++;
+        a.fu0[k] = u0; a.fnu[k] = nu; a.fv0[k] = v0; a.fnv[k] = nv;
+    };
+    add(0, top, 0, a.Vo);                 // rows above the interior, full width
+    add(a.Uo - bot, bot, 0, a.Vo);        // rows below
+    add(top, mid, 0, left);               // columns left of the interior
+    add(top, mid, a.Vo - right, right);   // columns right
+    a.fblk[0] = 0;
+    for (int k = 0; k < a.fseg; ++k)
+        a.fblk[k + 1] = a.fblk[k] + ((a.fnu[k] + kBH - 1) / kBH) * ((a.fnv[k] + kBW - 1) / kBW);
+}
+
 bool igemm_plan(IgemmArgs& a, int dtype) {
     a.kind = 0;
     // a merged-phase backward-data request runs on the register-weight kernel or not at all
     if (a.bp) return dtype == 1 && igemm_wreg_plan(a);
-    if (dtype == 1 && igemm_roll_plan(a)) return true;
-    if (dtype == 1 && igemm_wreg_plan(a)) return true;
-    if (dtype == 0 && igemm_f32w_plan(a)) return true;
+    // a frame runs on the chunked kernel (the strip kernels cover whole tiles)
+    if (!a.frame) {
+        if (dtype == 1 && igemm_roll_plan(a)) return true;
+        if (dtype == 1 && igemm_wreg_plan(a)) return true;
+        if (dtype == 0 && igemm_f32w_plan(a)) return true;
+    }
     a.OB = a.Cout <= 32 ? 32 : 64;
     // channel-chunk candidates, widest first: the channel count itself (rounded
     // to the k-granularity) when it is small, then powers of two
@@ -326,7 +372,8 @@ hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
     if (a.kind == 2) return launch_igemm_f32w(a, s);
     if (a.kind == 3) return launch_igemm_roll(a, s);
     const int nvb = (a.Vo + kBW - 1) / kBW, nub = (a.Uo + kBH - 1) / kBH;
-    dim3 grid(nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
+    dim3 grid(a.frame ? a.fblk[a.fseg] : nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
+    if (grid.x == 0) return hipSuccess;   // an empty frame
     dim3 block(kThreads);
     if (a.lds_bytes > 64 * 1024) {
         hipError_t e = hipSuccess;

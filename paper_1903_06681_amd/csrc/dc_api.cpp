@@ -98,12 +98,16 @@ dc_status make_geo(const dc_problem* p, Geo* g) {
     auto round16 = [&](int64_t e) { const int64_t a = 16 / g->esize; return (e + a - 1) / a * a; };
     g->x_halo = round16(int64_t(g->N) * g->C * halo_band_elems(g->bw_x, g->Ht, g->Wt));
     g->dy_halo = round16(int64_t(g->N) * g->K * halo_band_elems(g->bw_dy, g->Hot, g->Wot));
-    int64_t y_tile = int64_t(g->N) * g->K * g->Hot * g->Wot;
-    int64_t dx_tile = int64_t(g->N) * g->C * g->Ht * g->Wt;
-    int64_t w_elems = int64_t(g->K) * g->C * g->R * g->S;
-    if (g->x_tile > kMaxElems || g->dy_tile > kMaxElems || y_tile > kMaxElems ||
-        dx_tile > kMaxElems || w_elems > kMaxElems)
-        return DC_ERR_TOO_LARGE;
+    g->x_sample = int64_t(g->C) * g->x_rows * g->x_pitch;
+    g->dy_sample = int64_t(g->K) * g->dy_rows * g->dy_pitch;
+    g->y_sample = int64_t(g->K) * g->Hot * g->Wot;
+    g->dx_sample = int64_t(g->C) * g->Ht * g->Wt;
+    const int64_t w_elems = int64_t(g->K) * g->C * g->R * g->S;
+    const int64_t per_sample = std::max({g->x_sample, g->dy_sample, g->y_sample, g->dx_sample});
+    // the kernels index one launch's tile tensors with 32-bit element offsets:
+    // larger tiles are run in groups of samples (one sample must fit)
+    if (per_sample > kMaxElems || w_elems > kMaxElems) return DC_ERR_TOO_LARGE;
+    g->spg = int(std::min<int64_t>(g->N, kMaxElems / per_sample));
     return DC_OK;
 }
 
@@ -211,6 +215,44 @@ static void igemm_common(const Geo& g, int32_t tile, IgemmArgs& a) {
     a.Nn = g.N;
     a.R = g.R; a.S = g.S;
     a.wK = g.K; a.wC = g.C;
+}
+
+// One launch per group of g.spg samples (a single one unless the tile's
+// tensors exceed 32-bit indexing): the input and output pointers advance by
+// in_sample / out_sample elements per sample; tile strides stay those of the
+// whole tile.  Each launch is planned here; false if one cannot be.
+static bool plan_groups(const Geo& g, const IgemmArgs& a, int64_t in_sample, int64_t out_sample,
+                        std::vector<IgemmArgs>& out) {
+    const int64_t ebytes = g.esize;
+    for (int n0 = 0; n0 < g.N; n0 += g.spg) {
+        IgemmArgs ak = a;
+        ak.Nn = std::min(g.spg, g.N - n0);
+        ak.in = static_cast<const char*>(a.in) + n0 * in_sample * ebytes;
+        ak.out = a.out + n0 * out_sample;
+        if (!igemm_plan(ak, g.dtype)) return false;
+        out.push_back(ak);
+    }
+    return true;
+}
+
+// Workspace of the weight gradient: the largest of its sample groups' (they
+// run one after another on the stream and share it).
+static size_t bwd_filter_need(const Geo& g, int32_t tile) {
+    const int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
+    size_t need = 0;
+    for (int n0 = 0; n0 < g.N; n0 += g.spg)
+        need = std::max(need, wgrad_workspace_bytes(g.dtype, nt, std::min(g.spg, g.N - n0), g.C, g.K, g.R,
+                                                     g.S, g.stride, g.Hot, g.Wot, g.h - g.pad, g.h));
+    return need;
+}
+
+static dc_status launch_all(const std::vector<IgemmArgs>& v, int dtype, hipStream_t s) {
+    clear_stale_error();
+    for (const IgemmArgs& a : v) {
+        dc_status r = launched(launch_igemm(a, dtype, s));
+        if (r != DC_OK) return r;
+    }
+    return DC_OK;
 }
 
 }  // namespace dc
@@ -330,11 +372,19 @@ dc_status dc_halo_bands(const dc_problem* prob, int32_t which, int32_t bw[4]) {
 
 dc_status dc_conv_fwd(const dc_problem* prob, int32_t tile, const void* x_pad,
                       const void* w, float* y, void* stream) {
+    return dc_conv_fwd_region(prob, tile, DC_REGION_ALL, x_pad, w, y, stream);
+}
+
+dc_status dc_conv_fwd_region(const dc_problem* prob, int32_t tile, int32_t region, const void* x_pad,
+                             const void* w, float* y, void* stream) {
     Geo g;
     dc_status st = make_geo_tile(prob, tile, &g);
     if (st != DC_OK) return st;
+    if (region != DC_REGION_ALL && region != DC_REGION_INTERIOR && region != DC_REGION_BOUNDARY)
+        return DC_ERR_ARG;
     if (!x_pad || !w || !y) return DC_ERR_NULL;
     if (misaligned(x_pad) || misaligned(w) || misaligned(y)) return DC_ERR_ALIGN;
+    if (region != DC_REGION_ALL && g.stride != 1) return DC_ERR_UNSUPPORTED;
     IgemmArgs a;
     igemm_common(g, tile, a);
     a.in = x_pad; a.w = w; a.out = y;
@@ -351,18 +401,29 @@ dc_status dc_conv_fwd(const dc_problem* prob, int32_t tile, const void* x_pad,
     a.wr0 = 0; a.wrstep = 1; a.ws0 = 0; a.wsstep = 1;
     a.w_os = int64_t(g.C) * g.R * g.S; a.w_cs = int64_t(g.R) * g.S;
     a.wmode = 0;
-    if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
-    clear_stale_error();
-    return launched(launch_igemm(a, g.dtype, static_cast<hipStream_t>(stream)));
+    // stride 1: the outputs that read x's halo bands are the frame of those
+    // widths (output row p reads input rows p - pad .. p - pad + R - 1)
+    if (region == DC_REGION_BOUNDARY) igemm_set_frame(a, g.bw_x);
+    std::vector<IgemmArgs> launches;
+    if (!plan_groups(g, a, g.x_sample, g.y_sample, launches)) return DC_ERR_UNSUPPORTED;
+    return launch_all(launches, g.dtype, static_cast<hipStream_t>(stream));
 }
 
 dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_pad,
                            const void* w, float* dx, void* stream) {
+    return dc_conv_bwd_data_region(prob, tile, DC_REGION_ALL, dy_pad, w, dx, stream);
+}
+
+dc_status dc_conv_bwd_data_region(const dc_problem* prob, int32_t tile, int32_t region,
+                                  const void* dy_pad, const void* w, float* dx, void* stream) {
     Geo g;
     dc_status st = make_geo_tile(prob, tile, &g);
     if (st != DC_OK) return st;
+    if (region != DC_REGION_ALL && region != DC_REGION_INTERIOR && region != DC_REGION_BOUNDARY)
+        return DC_ERR_ARG;
     if (!dy_pad || !w || !dx) return DC_ERR_NULL;
     if (misaligned(dy_pad) || misaligned(w) || misaligned(dx)) return DC_ERR_ALIGN;
+    if (region != DC_REGION_ALL && g.stride != 1) return DC_ERR_UNSUPPORTED;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int st_ = g.stride;
     // Stride 2 with at most 8 channels: the four output phases below share
@@ -404,10 +465,9 @@ dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_
         a.bp = 1; a.bpC = g.C;
         a.w_os = int64_t(g.R) * g.S; a.w_cs = int64_t(g.C) * g.R * g.S;
         a.wmode = 0;
-        if (ok && a.base_r >= 0 && a.base_c >= 0 && igemm_plan(a, g.dtype)) {
-            clear_stale_error();
-            return launched(launch_igemm(a, g.dtype, s));
-        }
+        std::vector<IgemmArgs> launches;
+        if (ok && a.base_r >= 0 && a.base_c >= 0 && plan_groups(g, a, g.dy_sample, g.dx_sample, launches))
+            return launch_all(launches, g.dtype, s);
     }
     // Eq. (3) split by output phase (i mod stride, j mod stride): each phase
     // is a stride-1 correlation of dy with the taps r = (phase+pad) mod stride
@@ -439,26 +499,21 @@ dc_status dc_conv_bwd_data(const dc_problem* prob, int32_t tile, const void* dy_
             if (a.Tr == 0 || a.Ts == 0) { a.Tr = 0; a.Ts = 0; a.base_r = 0; a.base_c = 0; }
             a.w_os = int64_t(g.R) * g.S; a.w_cs = int64_t(g.C) * g.R * g.S;
             a.wmode = 1;
-            if (!igemm_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
-            phases.push_back(a);
+            // stride 1: the inputs whose gradient reads dy's halo bands are the
+            // frame of those widths (dx row i reads dy rows i + pad - R + 1 .. i + pad)
+            if (region == DC_REGION_BOUNDARY) igemm_set_frame(a, g.bw_dy);
+            if (!plan_groups(g, a, g.dy_sample, g.dx_sample, phases)) return DC_ERR_UNSUPPORTED;
         }
     }
     // every phase is planned before the first launch: an unsupported one
     // launches nothing
-    clear_stale_error();
-    for (const IgemmArgs& a : phases) {
-        dc_status r = launched(launch_igemm(a, g.dtype, s));
-        if (r != DC_OK) return r;
-    }
-    return DC_OK;
+    return launch_all(phases, g.dtype, s);
 }
 
 size_t dc_bwd_filter_workspace_bytes(const dc_problem* prob, int32_t tile) {
     Geo g;
     if (make_geo_tile(prob, tile, &g) != DC_OK) return 0;
-    int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
-    return wgrad_workspace_bytes(g.dtype, nt, g.N, g.C, g.K, g.R, g.S, g.stride, g.Hot, g.Wot,
-                                 g.h - g.pad, g.h);
+    return bwd_filter_need(g, tile);
 }
 
 }  // extern "C"
@@ -474,30 +529,40 @@ static dc_status bwd_filter_check(const dc_problem* prob, int32_t tile, const vo
     if (accumulate != 0 && accumulate != 1) return DC_ERR_ARG;
     if (!x_pad || !dy_pad || !dw) return DC_ERR_NULL;
     if (misaligned(x_pad) || misaligned(dy_pad) || misaligned(dw)) return DC_ERR_ALIGN;
-    const int nt = tile == DC_ALL_TILES ? g->ntiles : 1;
-    *need = wgrad_workspace_bytes(g->dtype, nt, g->N, g->C, g->K, g->R, g->S, g->stride, g->Hot,
-                                  g->Wot, g->h - g->pad, g->h);
+    *need = bwd_filter_need(*g, tile);
     return DC_OK;
 }
 
 static dc_status bwd_filter_launch(const Geo& g, int32_t tile, const void* x_pad, const void* dy_pad,
                                    float* dw, int32_t accumulate, void* workspace, void* stream) {
     const int nt = tile == DC_ALL_TILES ? g.ntiles : 1;
-    WgradArgs a;
-    std::memset(&a, 0, sizeof(a));
-    a.x = x_pad; a.dy = dy_pad; a.part = static_cast<float*>(workspace); a.dw = dw;
-    a.x_tile = g.x_tile; a.dy_tile = g.dy_tile;
-    a.ntiles = nt; a.Nn = g.N;
-    a.C = g.C; a.K = g.K; a.R = g.R; a.S = g.S;
-    a.x_rows = g.x_rows; a.x_cols = g.x_cols; a.x_pitch = g.x_pitch;
-    a.dy_pitch = g.dy_pitch; a.dy_off = g.h;
-    a.Hot = g.Hot; a.Wot = g.Wot;
-    a.istr = g.stride;
-    a.base_r = g.h - g.pad; a.base_c = g.h - g.pad;
-    a.accumulate = accumulate;
-    if (!wgrad_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+    // sample groups (one unless the tile exceeds 32-bit indexing) in order,
+    // each adding its partial to dw after the first: a fixed summation order
+    std::vector<WgradArgs> launches;
+    for (int n0 = 0; n0 < g.N; n0 += g.spg) {
+        WgradArgs a;
+        std::memset(&a, 0, sizeof(a));
+        a.x = static_cast<const char*>(x_pad) + n0 * g.x_sample * g.esize;
+        a.dy = static_cast<const char*>(dy_pad) + n0 * g.dy_sample * g.esize;
+        a.part = static_cast<float*>(workspace); a.dw = dw;
+        a.x_tile = g.x_tile; a.dy_tile = g.dy_tile;
+        a.ntiles = nt; a.Nn = std::min(g.spg, g.N - n0);
+        a.C = g.C; a.K = g.K; a.R = g.R; a.S = g.S;
+        a.x_rows = g.x_rows; a.x_cols = g.x_cols; a.x_pitch = g.x_pitch;
+        a.dy_pitch = g.dy_pitch; a.dy_off = g.h;
+        a.Hot = g.Hot; a.Wot = g.Wot;
+        a.istr = g.stride;
+        a.base_r = g.h - g.pad; a.base_c = g.h - g.pad;
+        a.accumulate = n0 == 0 ? accumulate : 1;
+        if (!wgrad_plan(a, g.dtype)) return DC_ERR_UNSUPPORTED;
+        launches.push_back(a);
+    }
     clear_stale_error();
-    return launched(launch_wgrad(a, g.dtype, static_cast<hipStream_t>(stream)));
+    for (const WgradArgs& a : launches) {
+        dc_status r = launched(launch_wgrad(a, g.dtype, static_cast<hipStream_t>(stream)));
+        if (r != DC_OK) return r;
+    }
+    return DC_OK;
 }
 
 }  // namespace dc

@@ -26,6 +26,10 @@ struct Geo {
     int need_dy_lo_r, need_dy_hi_r, need_dy_lo_s, need_dy_hi_s;
     // halo bands moved by pack/unpack: rows above, below, cols left, right
     int bw_x[4], bw_dy[4];
+    // convolution launches take the samples in groups of spg, so that each
+    // launch's per-tile tensors stay within 32-bit element indexing
+    int spg;
+    int64_t x_sample, dy_sample, y_sample, dx_sample;   // elements per sample of each tile tensor
 };
 
 // Fill g from prob and check everything that does not depend on a tile index.

@@ -87,10 +87,20 @@ struct IgemmArgs {
     int bp, bpC, bpvoff;
     int bpdr[2], bptr[2], bpr0[2], bpdc[2], bpts[2], bps0[2];
     int nvb, nseg, rows_per_seg; // strip kernels: 64- (128-, rolling) column strips, row segments
+    // frame mode (chunked kernels only): the launch covers only the output
+    // rectangles [fu0, fu0 + fnu) x [fv0, fv0 + fnv) of fseg segments, whose
+    // workgroups are numbered from fblk[seg] (prefix sums, fblk[fseg] total)
+    int frame, fseg;
+    int fu0[4], fv0[4], fnu[4], fnv[4], fblk[5];
 };
 
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
 int device_lds_limit();
+
+// Frame mode: the output rows above / below and columns left / right of the
+// interior, of widths bands[0..3] (clamped to the Uo x Vo output), as the
+// segments of one launch of the chunked kernel.
+void igemm_set_frame(IgemmArgs& a, const int bands[4]);
 
 // Chooses the channel chunk and LDS size; returns false if no variant fits.
 bool igemm_plan(IgemmArgs& a, int dtype);

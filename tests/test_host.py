@@ -226,3 +226,22 @@ def test_noalloc_bwd_filter_limit_matches_header_and_rejects_larger_problems():
     assert dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(p), 0, A16, A32, A48, 2, None) == -10
     assert dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(p), 0, A16, None, A48, 0, None) == -1
     assert dc.lib().dc_conv_bwd_filter_noalloc(ctypes.byref(p), 0, A16, A32, MIS, 0, None) == -7
+
+
+def test_region_calls_checked_before_launch():
+    p = prob()
+    assert _status(dc.conv_fwd_region, p, 0, 3, A16, A32, A48, 0) == -10
+    assert _status(dc.conv_bwd_data_region, p, 0, -1, A16, A32, A48, 0) == -10
+    s2 = prob(stride=2)
+    assert _status(dc.conv_fwd_region, s2, 0, dc.DC_REGION_BOUNDARY, A16, A32, A48, 0) == -5
+    assert _status(dc.conv_bwd_data_region, s2, 0, dc.DC_REGION_INTERIOR, A16, A32, A48, 0) == -5
+    assert _status(dc.conv_fwd_region, p, 0, dc.DC_REGION_INTERIOR, None, A32, A48, 0) == -1
+
+
+def test_tiles_beyond_32bit_indexing_validate_single_samples_must_fit():
+    big = prob(N=32, C=64, K=64, H=1024, W=1024, P=1, Q=1, dtype=dc.DC_BF16)
+    assert dc.tile_elems(big, dc.DC_X) > 2**31          # run in groups of samples
+    assert dc.validate(big, 0) == 0
+    assert dc.bwd_filter_workspace_bytes(big, 0) > 0
+    huge = prob(N=1, C=2048, K=64, H=1024, W=1024, P=1, Q=1, dtype=dc.DC_BF16)
+    assert dc.validate(huge, 0) == -11                   # one sample alone is too large
