@@ -528,8 +528,8 @@ def main():
         dc.halo_pack(p, tile, DY, dyp, send_dy, sb)
         dc.halo_unpack(p, tile, DY, recv_dy, dyp, sb)
         ev_dy.record(stream_b)
-        dc.conv_bwd_filter(p, tile, xp, dyp, dw, 0, ws, sh)
         dc.conv_bwd_data_region(p, tile, RI, dyp, wd, dx, sh)
+        dc.conv_bwd_filter(p, tile, xp, dyp, dw, 0, ws, sh)
         stream.wait_event(ev_dy)
         dc.conv_bwd_data_region(p, tile, RB, dyp, wd, dx, sh)
 

@@ -40,26 +40,39 @@ __host__ __device__ inline int bf16_pixel_stride(int CC) { return 8 * ((CC / 8) 
 
 // fp32 patch plane stride (floats): rows*cols rounded up to 32 mod 64, so the
 // two half-waves (adjacent channels, same pixels) use disjoint banks.
-__host__ __device__ inline int f32_plane_stride(int PR, int PC) {
-    int p = PR * PC;
+__host__ __device__ inline int f32_plane_stride(int p) {
     int r = p % 64;
     return r <= 32 ? p + (32 - r) : p + (96 - r);
+}
+
+// Pixels of a workgroup's input patch: kBH x kBW output block, or in frame
+// mode the larger of that and its transpose (column segments).
+__host__ __device__ inline int patch_pixels(const IgemmArgs& a) {
+    const int rm = ((kBH - 1) * a.istr + a.Tr) * ((kBW - 1) * a.istr + a.Ts);
+    const int cm = ((kBW - 1) * a.istr + a.Tr) * ((kBH - 1) * a.istr + a.Ts);
+    return a.frame && cm > rm ? cm : rm;
 }
 
 
 // Output block of this workgroup: kBH rows x kBW columns from (u0, v0), with
 // stores limited to rows < uend and columns < vend.  Whole tile: blocks in
 // row-major order over Uo x Vo.  Frame mode: blocks of the segments in turn,
-// each a rectangle of the output (the boundary band of a tile).
-__device__ __forceinline__ void block_origin(const IgemmArgs& a, int& u0, int& v0, int& uend, int& vend) {
+// each a rectangle of the output (the boundary band of a tile); the blocks of
+// a column segment (cm) are kBW rows x kBH columns, wave w then owning output
+// column w and its MFMA pixels running down the rows.
+__device__ __forceinline__ void block_origin(const IgemmArgs& a, int& u0, int& v0, int& uend, int& vend,
+                                             bool& cm) {
+    cm = false;
     if (a.frame) {
         int sg = 0;
         while (sg + 1 < a.fseg && int(blockIdx.x) >= a.fblk[sg + 1]) ++sg;
         const int local = blockIdx.x - a.fblk[sg];
-        const int nvb = (a.fnv[sg] + kBW - 1) / kBW;
+        cm = a.fcm[sg] != 0;   // column segment: blocks of kBW rows x kBH columns
+        const int bw = cm ? kBH : kBW, bh = cm ? kBW : kBH;
+        const int nvb = (a.fnv[sg] + bw - 1) / bw;
         const int vb = local % nvb, ub = local / nvb;
-        u0 = a.fu0[sg] + ub * kBH;
-        v0 = a.fv0[sg] + vb * kBW;
+        u0 = a.fu0[sg] + ub * bh;
+        v0 = a.fv0[sg] + vb * bw;
         uend = a.fu0[sg] + a.fnu[sg];
         vend = a.fv0[sg] + a.fnv[sg];
     } else {
@@ -76,17 +89,18 @@ template <int OB>
 __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int NOB = OB / 32;
+    int u0, v0, uend, vend;
+    bool cm;
+    block_origin(a, u0, v0, uend, vend, cm);
     const int CC = a.CC, CCG = CC / 8;
     const int Tt = a.Tr * a.Ts;
     const int G = Tt * CCG;
-    const int PR = (kBH - 1) * a.istr + a.Tr;
-    const int PC = (kBW - 1) * a.istr + a.Ts;
+    const int PR = ((cm ? kBW : kBH) - 1) * a.istr + a.Tr;
+    const int PC = ((cm ? kBH : kBW) - 1) * a.istr + a.Ts;
     const int PS = bf16_pixel_stride(CC);
     uint16_t* wl = reinterpret_cast<uint16_t*>(smem);   // [G][OB][8]
     uint16_t* pl = wl + G * OB * 8;                      // [PR][PC][PS]
 
-    int u0, v0, uend, vend;
-    block_origin(a, u0, v0, uend, vend);
     const int o0 = blockIdx.y * OB;
     const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
 
@@ -154,10 +168,10 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
 #pragma unroll
                 for (int ob = 0; ob < NOB; ++ob)
                     A[ob] = *reinterpret_cast<const bf16x8*>(wl + (g * OB + ob * 32 + l32) * 8);
-                const int prow = wave * a.istr + tr;
 #pragma unroll
                 for (int pb = 0; pb < 2; ++pb) {
-                    const int pcol = (pb * 32 + l32) * a.istr + ts;
+                    const int pm = (pb * 32 + l32) * a.istr, pw = wave * a.istr;
+                    const int prow = (cm ? pm : pw) + tr, pcol = (cm ? pw : pm) + ts;
                     B[pb] = *reinterpret_cast<const bf16x8*>(pl + (prow * PC + pcol) * PS + cb * 8);
                 }
             } else {
@@ -180,16 +194,15 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
 
     // D layout of a 32x32 MFMA tile: value i of lane l is row 8*(i/4) + 4*(l/32) + i%4,
     // column l%32.  Rows are output channels, columns pixels.
-    const int u = u0 + wave;
-    if (u >= uend) return;
     float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
-    const int orow = u * a.ostr + a.oph_r;
 #pragma unroll
     for (int ob = 0; ob < NOB; ++ob)
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
-            const int v = v0 + pb * 32 + l32;
-            if (v >= vend) continue;
+            const int u = cm ? u0 + pb * 32 + l32 : u0 + wave;
+            const int v = cm ? v0 + wave : v0 + pb * 32 + l32;
+            if (u >= uend || v >= vend) continue;
+            const int orow = u * a.ostr + a.oph_r;
             const int ocol = v * a.ostr + a.oph_c;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -204,17 +217,18 @@ template <int OB>
 __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int NOB = OB / 32;
+    int u0, v0, uend, vend;
+    bool cm;
+    block_origin(a, u0, v0, uend, vend, cm);
     const int CC = a.CC;
     const int Tt = a.Tr * a.Ts;
     const int KG = Tt * CC;
-    const int PR = (kBH - 1) * a.istr + a.Tr;
-    const int PC = (kBW - 1) * a.istr + a.Ts;
-    const int PLN = f32_plane_stride(PR, PC);
+    const int PR = ((cm ? kBW : kBH) - 1) * a.istr + a.Tr;
+    const int PC = ((cm ? kBH : kBW) - 1) * a.istr + a.Ts;
+    const int PLN = f32_plane_stride(patch_pixels(a));
     float* wl = reinterpret_cast<float*>(smem);   // [KG][OB]
     float* pl = wl + KG * OB;                     // [CC][PLN] with rows of PC
 
-    int u0, v0, uend, vend;
-    block_origin(a, u0, v0, uend, vend);
     const int o0 = blockIdx.y * OB;
     const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
 
@@ -264,10 +278,12 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
                 const int tr = t / a.Ts, ts = t - tr * a.Ts;
 #pragma unroll
                 for (int ob = 0; ob < NOB; ++ob) A[ob] = wl[kg * OB + ob * 32 + l32];
-                const int prow = wave * a.istr + tr;
 #pragma unroll
-                for (int pb = 0; pb < 2; ++pb)
-                    B[pb] = pl[cl * PLN + prow * PC + (pb * 32 + l32) * a.istr + ts];
+                for (int pb = 0; pb < 2; ++pb) {
+                    const int pm = (pb * 32 + l32) * a.istr, pw = wave * a.istr;
+                    const int prow = (cm ? pm : pw) + tr, pcol = (cm ? pw : pm) + ts;
+                    B[pb] = pl[cl * PLN + prow * PC + pcol];
+                }
             } else {
 #pragma unroll
                 for (int ob = 0; ob < NOB; ++ob) A[ob] = 0.f;
@@ -281,16 +297,15 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
         }
     }
 
-    const int u = u0 + wave;
-    if (u >= uend) return;
     float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
-    const int orow = u * a.ostr + a.oph_r;
 #pragma unroll
     for (int ob = 0; ob < NOB; ++ob)
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
-            const int v = v0 + pb * 32 + l32;
-            if (v >= vend) continue;
+            const int u = cm ? u0 + pb * 32 + l32 : u0 + wave;
+            const int v = cm ? v0 + wave : v0 + pb * 32 + l32;
+            if (u >= uend || v >= vend) continue;
+            const int orow = u * a.ostr + a.oph_r;
             const int ocol = v * a.ostr + a.oph_c;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
@@ -302,14 +317,12 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
 }
 
 static int lds_bytes_for(const IgemmArgs& a, int dtype, int CC, int OB) {
-    const int PR = (kBH - 1) * a.istr + a.Tr;
-    const int PC = (kBW - 1) * a.istr + a.Ts;
     const int Tt = a.Tr * a.Ts;
     if (dtype == 1) {
         const int G = Tt * (CC / 8);
-        return G * OB * 16 + PR * PC * bf16_pixel_stride(CC) * 2;
+        return G * OB * 16 + patch_pixels(a) * bf16_pixel_stride(CC) * 2;
     }
-    return (Tt * CC * OB + CC * f32_plane_stride(PR, PC)) * 4;
+    return (Tt * CC * OB + CC * f32_plane_stride(patch_pixels(a))) * 4;
 }
 
 void igemm_set_frame(IgemmArgs& a, const int bands[4]) {
@@ -318,18 +331,20 @@ void igemm_set_frame(IgemmArgs& a, const int bands[4]) {
     const int top = std::min(bands[0], a.Uo), bot = std::min(bands[1], a.Uo - top);
     const int mid = a.Uo - top - bot;
     const int left = std::min(bands[2], a.Vo), right = std::min(bands[3], a.Vo - left);
-    auto add = [&](int u0, int nu, int v0, int nv) {
+    auto add = [&](int u0, int nu, int v0, int nv, int cm) {
         if (nu <= 0 || nv <= 0) return;
         const int k = a.fseg++;
-        a.fu0[k] = u0; a.fnu[k] = nu; a.fv0[k] = v0; a.fnv[k] = nv;
+        a.fu0[k] = u0; a.fnu[k] = nu; a.fv0[k] = v0; a.fnv[k] = nv; a.fcm[k] = cm;
     };
-    add(0, top, 0, a.Vo);                 // rows above the interior, full width
-    add(a.Uo - bot, bot, 0, a.Vo);        // rows below
-    add(top, mid, 0, left);               // columns left of the interior
-    add(top, mid, a.Vo - right, right);   // columns right
+    add(0, top, 0, a.Vo, 0);                 // rows above the interior, full width
+    add(a.Uo - bot, bot, 0, a.Vo, 0);        // rows below
+    add(top, mid, 0, left, 1);               // columns left of the interior
+    add(top, mid, a.Vo - right, right, 1);   // columns right
     a.fblk[0] = 0;
-    for (int k = 0; k < a.fseg; ++k)
-        a.fblk[k + 1] = a.fblk[k] + ((a.fnu[k] + kBH - 1) / kBH) * ((a.fnv[k] + kBW - 1) / kBW);
+    for (int k = 0; k < a.fseg; ++k) {
+        const int bh = a.fcm[k] ? kBW : kBH, bw = a.fcm[k] ? kBH : kBW;
+        a.fblk[k + 1] = a.fblk[k] + ((a.fnu[k] + bh - 1) / bh) * ((a.fnv[k] + bw - 1) / bw);
+    }
 }
 
 bool igemm_plan(IgemmArgs& a, int dtype) {

@@ -91,7 +91,7 @@ struct IgemmArgs {
     // rectangles [fu0, fu0 + fnu) x [fv0, fv0 + fnv) of fseg segments, whose
     // workgroups are numbered from fblk[seg] (prefix sums, fblk[fseg] total)
     int frame, fseg;
-    int fu0[4], fv0[4], fnu[4], fnv[4], fblk[5];
+    int fu0[4], fv0[4], fnu[4], fnv[4], fcm[4], fblk[5];
 };
 
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
