@@ -335,6 +335,21 @@ def format_table(layer: LayerShape, gpus: int, preds: List[Prediction],
     return "\n".join(lines)
 
 
+def source_digest() -> str:
+    """sha256 over the library's kernel and host sources (the timings belong to them)."""
+    import hashlib
+    import os
+
+    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
 def main(argv: Optional[List[str]] = None) -> None:
     """python -m paper_1903_06681_amd.perfmodel: measure and rank the splits
     of a few layers on the current GPU."""
@@ -347,11 +362,14 @@ def main(argv: Optional[List[str]] = None) -> None:
     ap.add_argument("--latency-us", type=float, default=10.0)
     args = ap.parse_args(argv)
     link = xgmi_link(args.link_gbps, args.latency_us * 1e-6)
+    print(f"source_sha256: {source_digest()}", flush=True)
     layers = {
         # ResNet-50 stage-2 3x3 layer, mini-batch 32 (Sec. VI-A microbenchmarks)
         "3x3 64->64 56x56, N=32": LayerShape(32, 64, 64, 56, 56, 3, 3, 1, 1, 1, "bf16"),
         # large-sample layer: 3x3 64->64 on 1024x1024, mini-batch 32
         "3x3 64->64 1024x1024, N=32": LayerShape(32, 64, 64, 1024, 1024, 3, 3, 1, 1, 1, "bf16"),
+        # the same layer with 4 samples: its 1 x 4 x 4 split is the benchmark's tile
+        "3x3 64->64 1024x1024, N=4": LayerShape(4, 64, 64, 1024, 1024, 3, 3, 1, 1, 1, "bf16"),
         # mesh-model first layer: 18 -> 32 channels on 2048x2048 fp32, one sample per step
         "3x3 18->32 2048x2048 fp32, N=1": LayerShape(1, 18, 32, 2048, 2048, 3, 3, 1, 1, 1, "f32"),
     }
