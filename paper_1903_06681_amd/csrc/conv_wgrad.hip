@@ -36,6 +36,7 @@
 
 namespace dc {
 
+typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 static constexpr int kThreads = 256;
 static constexpr int kBQ = 64;          // output columns staged per step
@@ -909,7 +910,11 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
         });
         __syncthreads();
     });
-    // partial, [chunk][block][unit][64 lanes][4]: this wave's units
+    // partial, [chunk][block][unit][64 lanes][4]: this wave's units.  The
+    // partials are stored at device scope (sc1, written through): the reduce
+    // launch reads them from another XCD anyway, and the kernel then ends with
+    // no dirty lines for the end-of-kernel L2 write-back (about 1 us less per
+    // pass on a 64-channel 3x3 layer than plain write-back stores).
     float4* part = reinterpret_cast<float4*>(a.part + int64_t(blockIdx.x) * a.F +
                                              int64_t(blockIdx.z) * NT * 1024) + lane;
     static_for<0, NW>([&](auto kc) {
@@ -919,7 +924,9 @@ __global__ __launch_bounds__(64 * NW) void wgrad_kslice_bf16_kernel(WgradArgs a)
             static_for<LO, HI>([&](auto uc) {
                 constexpr int u = decltype(uc)::value, q = u % 4;
                 const floatx16& v = acc[u / 4];
-                part[u * 64] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+                const f32x4v val = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+                float4* dst = part + u * 64;
+                asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(dst), "v"(val) : "memory");
             });
     });
 }
