@@ -11,6 +11,11 @@
 // a compile-time offset.  Each lane keeps its A values (one per k-step) in
 // registers for the whole launch.
 //
+// The kernel is compiled for a channel capacity CC (a class: multiples of 4
+// up to 32, and 18, the mesh layer's count) and runs any channel count
+// C <= CC: channels C .. CC-1 get zero weights and zero-filled ring rows, so
+// they add nothing (at most three per k-step group; none for C = CC).
+//
 // A workgroup (4 waves) walks down a 64-column strip of one sample, two
 // output rows per step (wave w: row w / 2, pixels 32 * (w % 2) .. + 31); input
 // rows live in an LDS ring stored channel-major ([row][channel][column]).
@@ -40,7 +45,7 @@ struct F32WGeom {
 
 }  // namespace
 
-template <int CIN, int TR, int TS>
+template <int CIN, int TR, int TS>   // CIN: the channel capacity, a.Cin <= CIN
 __global__ __launch_bounds__(kF32WThreads, 1) void igemm_f32w_kernel(IgemmArgs a) {
     using G = F32WGeom<TS>;
     constexpr int T = TR * TS;
@@ -67,7 +72,8 @@ __global__ __launch_bounds__(kF32WThreads, 1) void igemm_f32w_kernel(IgemmArgs a
     const int wrow = wave >> 1, pb = wave & 1;
 
     const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
-    const float* in = static_cast<const float*>(a.in) + tile * a.in_tile + int64_t(n) * CIN * plane;
+    const int cin = a.Cin;
+    const float* in = static_cast<const float*>(a.in) + tile * a.in_tile + int64_t(n) * cin * plane;
     const int xr0 = u0 + a.base_r;   // input row of ring row 0
     const int xc0 = v0 + a.base_c;   // input column of staged column 0 (a multiple of 4)
 
@@ -82,8 +88,9 @@ __global__ __launch_bounds__(kF32WThreads, 1) void igemm_f32w_kernel(IgemmArgs a
             constexpr int j = decltype(jc)::value;
             constexpr int t = j / (CIN / 2), cp = j % (CIN / 2), tr = t / TS, ts = t % TS;
             const int ci = 2 * cp + hi;
-            const float v = w[wo + ci * a.w_cs + (a.wr0 + a.wrstep * tr) * a.S + (a.ws0 + a.wsstep * ts)];
-            A[j] = ok ? v : 0.f;
+            const bool oki = ok && ci < cin;
+            const float v = w[wo + (oki ? ci : 0) * a.w_cs + (a.wr0 + a.wrstep * tr) * a.S + (a.ws0 + a.wsstep * ts)];
+            A[j] = oki ? v : 0.f;
         });
     }
 
@@ -97,7 +104,8 @@ __global__ __launch_bounds__(kF32WThreads, 1) void igemm_f32w_kernel(IgemmArgs a
             const int ci = rem / G::V4, g = rem % G::V4;
             const int gr = min(max(xr0 + m0 + q, 0), a.in_rows - 1);
             const int gc = min(xc0 + 4 * g, a.in_pitch - 4);
-            stg[k] = *reinterpret_cast<const f32x4*>(in + ci * plane + int64_t(gr) * a.in_pitch + gc);
+            stg[k] = ci < cin ? *reinterpret_cast<const f32x4*>(in + ci * plane + int64_t(gr) * a.in_pitch + gc)
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
         });
     };
     auto store_rows = [&](int m0) {
@@ -162,14 +170,15 @@ __global__ __launch_bounds__(kF32WThreads, 1) void igemm_f32w_kernel(IgemmArgs a
 
 // ---------------------------------------------------------------- planning
 
-static bool f32w_shape(int CIN, int TR, int TS) {
-    // instantiated shapes (see launch_igemm_f32w)
-    const int shapes[][3] = {{18, 3, 3}, {32, 3, 3}, {4, 3, 3}, {8, 3, 3}, {16, 3, 3},
-                             {6, 1, 1}, {10, 1, 1}};
-    for (auto& s : shapes)
-        if (s[0] == CIN && s[1] == TR && s[2] == TS) return true;
-    return false;
+// Channel capacity class of a layer with C input channels (0: none): the
+// smallest of 4, 8, .., 32 that holds C, and 18 for the mesh layer's 17-18.
+static int f32w_class(int C) {
+    if (C < 1 || C > 32) return 0;
+    if (C == 17 || C == 18) return 18;
+    return (C + 3) / 4 * 4;
 }
+// filters the kernel is instantiated for: 3x3 and 1x1
+static bool f32w_filter(int TR, int TS) { return (TR == 3 && TS == 3) || (TR == 1 && TS == 1); }
 
 static int f32w_lds(int CIN, int TR, int TS) {
     const int XW = 64 + TS - 1, XWP = (XW + 3) / 4 * 4 + 4;
@@ -177,10 +186,11 @@ static int f32w_lds(int CIN, int TR, int TS) {
 }
 
 bool igemm_f32w_plan(IgemmArgs& a) {
-    if (a.istr != 1 || a.Cin % 2 != 0 || a.Tr < 1 || a.Ts < 1) return false;
+    if (a.istr != 1 || a.Tr < 1 || a.Ts < 1) return false;
     if (a.base_c % 4 != 0 || a.in_pitch % 4 != 0) return false;   // 16-byte aligned row loads
-    if (!f32w_shape(a.Cin, a.Tr, a.Ts)) return false;
-    const int lds = f32w_lds(a.Cin, a.Tr, a.Ts);
+    const int cc = f32w_class(a.Cin);
+    if (cc == 0 || !f32w_filter(a.Tr, a.Ts)) return false;
+    const int lds = f32w_lds(cc, a.Tr, a.Ts);
     if (lds > device_lds_limit()) return false;
     a.OB = 32;
     a.nvb = (a.Vo + 63) / 64;
@@ -212,15 +222,13 @@ static hipError_t launch_f32w(const IgemmArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s) {
+    const int cc = f32w_class(a.Cin);
 #define DC_F32W(cin, tr, ts) \
-    if (a.Cin == cin && a.Tr == tr && a.Ts == ts) return launch_f32w<cin, tr, ts>(a, s);
-    DC_F32W(18, 3, 3)
-    DC_F32W(32, 3, 3)
-    DC_F32W(4, 3, 3)
-    DC_F32W(8, 3, 3)
-    DC_F32W(16, 3, 3)
-    DC_F32W(6, 1, 1)
-    DC_F32W(10, 1, 1)
+    if (cc == cin && a.Tr == tr && a.Ts == ts) return launch_f32w<cin, tr, ts>(a, s);
+    DC_F32W(4, 3, 3) DC_F32W(8, 3, 3) DC_F32W(12, 3, 3) DC_F32W(16, 3, 3) DC_F32W(18, 3, 3)
+    DC_F32W(20, 3, 3) DC_F32W(24, 3, 3) DC_F32W(28, 3, 3) DC_F32W(32, 3, 3)
+    DC_F32W(4, 1, 1) DC_F32W(8, 1, 1) DC_F32W(12, 1, 1) DC_F32W(16, 1, 1) DC_F32W(18, 1, 1)
+    DC_F32W(20, 1, 1) DC_F32W(24, 1, 1) DC_F32W(28, 1, 1) DC_F32W(32, 1, 1)
 #undef DC_F32W
     return hipErrorInvalidValue;
 }

@@ -112,12 +112,16 @@ static bool kslice_offsets_fit(int C, int K, int R, int S, int Hot, int Wot) {
     const int64_t rows = 3 * (int64_t(Hot) + R + 8), cols = 3 * (int64_t(Wot) + S + 16);
     return 2 * int64_t(std::max(C, K)) * rows * cols < (int64_t(1) << 32);
 }
-// fp32 flattened-column kernel: instantiated (C, R, S)
+// fp32 flattened-column kernel: compiled for a channel capacity class (the
+// smallest of 4, 8, .., 32 that holds C, and 18 for the mesh layer's 17-18;
+// 0: none) and 3x3 or 1x1 filters; it runs any C up to its class
+static int f32w_class(int C) {
+    if (C < 1 || C > 32) return 0;
+    if (C == 17 || C == 18) return 18;
+    return (C + 3) / 4 * 4;
+}
 static bool f32w_shape(int C, int R, int S) {
-    const int shapes[][3] = {{18, 3, 3}, {4, 3, 3}, {8, 3, 3}, {5, 3, 3}, {6, 1, 1}, {16, 3, 3}};
-    for (auto& s : shapes)
-        if (s[0] == C && s[1] == R && s[2] == S) return true;
-    return false;
+    return f32w_class(C) > 0 && ((R == 3 && S == 3) || (R == 1 && S == 1));
 }
 static int f32w_lds(int C, int R, int S) {
     const int XW = 64 + S - 1 + 3, XWP = (XW + 3) / 4 * 4 + 4, DYP = 17 * 4 + 4;
@@ -236,7 +240,7 @@ bool wgrad_plan(WgradArgs& a, int dtype) {
     a.nqb = pl.nqb; a.nseg = pl.nseg; a.rows_per_seg = pl.rows_per_seg;
     a.F = pl.F; a.frag = pl.frag;
     if (a.kind == WGRAD_F32W) {
-        a.lds_bytes = f32w_lds(a.C, a.R, a.S);
+        a.lds_bytes = f32w_lds(f32w_class(a.C), a.R, a.S);
     } else if (a.kind == WGRAD_KSLICE_BF16) {
         // the staging buffers; after the loop the waves' sums (NW/2 of them at once)
         const int bufs = KsliceGeom<kKsliceNW>::loop_lds;
@@ -1204,10 +1208,15 @@ template <int S_> struct F32WgGeom {
 };
 }  // namespace
 
+// CIN is the channel capacity: channels a.C .. CIN-1 are staged as zeros,
+// and only the nb = ceil(a.C R S / 32) column blocks that hold real columns
+// are written (blocks past them repeat the last real column; a branch per
+// block in the MFMA loop cost the mesh layer 4 us)
 template <int CIN, int RR, int SS>
 __global__ __launch_bounds__(kThreads, 1) void wgrad_f32w_kernel(WgradArgs a) {
     using G = F32WgGeom<SS>;
     constexpr int CRS = CIN * RR * SS, NB = (CRS + 31) / 32;
+    const int crs = a.C * RR * SS, nb = (crs + 31) / 32;
     constexpr int NRX = RR + 1;                             // x ring slots
     constexpr int XSL = CIN * G::XWP;                       // floats per x slot
     constexpr int XUN = CIN * G::XV, DUN = 32 * G::DV;      // 16-byte units per x / dy row
@@ -1247,8 +1256,9 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_f32w_kernel(WgradArgs a) {
             constexpr int k = decltype(kc)::value;
             const int u = min(tid + k * kThreads, XUN - 1);
             const int ci = u / G::XV, g = u % G::XV;
-            xs[k] = *reinterpret_cast<const f32x4w*>(xt + ci * xplane + int64_t(gr) * a.x_pitch +
-                                                     min(xa + 4 * g, a.x_pitch - 4));
+            xs[k] = ci < a.C ? *reinterpret_cast<const f32x4w*>(xt + ci * xplane + int64_t(gr) * a.x_pitch +
+                                                                min(xa + 4 * g, a.x_pitch - 4))
+                             : f32x4w{0.f, 0.f, 0.f, 0.f};
         });
     };
     auto store_x = [&](int m) {   // zero outside the tile: padding columns feed masked pixels
@@ -1293,7 +1303,7 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_f32w_kernel(WgradArgs a) {
     int boff[NB], brow[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-        const int col = min(32 * b + l32, CRS - 1);   // columns past CRS are never stored
+        const int col = min(32 * b + l32, crs - 1);   // columns past crs are never stored
         const int ci = col / (RR * SS), r = (col / SS) % RR, sx = col % SS;
         boff[b] = ci * G::XWP + xsh + sx;
         brow[b] = r;
@@ -1343,8 +1353,8 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_f32w_kernel(WgradArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) red[((wave * NB + b) * 16 + e) * 64 + lane] = acc[b][e];
     __syncthreads();
-    float* part = a.part + int64_t(blockIdx.x) * a.F + int64_t(blockIdx.z) * NB * 1024;
-    for (int f = tid; f < NB * 1024; f += kThreads)
+    float* part = a.part + int64_t(blockIdx.x) * a.F + int64_t(blockIdx.z) * nb * 1024;
+    for (int f = tid; f < nb * 1024; f += kThreads)
         part[f] = ((red[f] + red[NB * 1024 + f]) + red[2 * NB * 1024 + f]) + red[3 * NB * 1024 + f];
 }
 
@@ -1536,10 +1546,13 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
         return hipErrorInvalidValue;
 #undef DC_STRIP
     } else if (a.kind == WGRAD_F32W) {
+        const int cc = f32w_class(a.C);
 #define DC_F32WG(c, r, s_) \
-        if (a.C == c && a.R == r && a.S == s_) e = launch_f32wg<c, r, s_>(a, grid, s); else
-        DC_F32WG(18, 3, 3) DC_F32WG(4, 3, 3) DC_F32WG(8, 3, 3) DC_F32WG(5, 3, 3) DC_F32WG(6, 1, 1)
-        DC_F32WG(16, 3, 3)
+        if (cc == c && a.R == r && a.S == s_) e = launch_f32wg<c, r, s_>(a, grid, s); else
+        DC_F32WG(4, 3, 3) DC_F32WG(8, 3, 3) DC_F32WG(12, 3, 3) DC_F32WG(16, 3, 3) DC_F32WG(18, 3, 3)
+        DC_F32WG(20, 3, 3) DC_F32WG(24, 3, 3) DC_F32WG(28, 3, 3) DC_F32WG(32, 3, 3)
+        DC_F32WG(4, 1, 1) DC_F32WG(8, 1, 1) DC_F32WG(12, 1, 1) DC_F32WG(16, 1, 1) DC_F32WG(18, 1, 1)
+        DC_F32WG(20, 1, 1) DC_F32WG(24, 1, 1) DC_F32WG(28, 1, 1) DC_F32WG(32, 1, 1)
         return hipErrorInvalidValue;
 #undef DC_F32WG
     } else if (a.kind == WGRAD_KSLICE_BF16) {

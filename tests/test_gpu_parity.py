@@ -120,6 +120,14 @@ SMALL = {
     "roll5c_bf16": Layer("roll5c_bf16", 1, 32, 32, 96, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 106),
     "roll5d_bf16": Layer("roll5d_bf16", 1, 32, 32, 112, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 107),
     "roll5e_bf16": Layer("roll5e_bf16", 1, 32, 32, 81, 128, 5, 5, 1, 2, 1, 1, 2, "bf16", "uniform", 108),
+    # fp32 register-weight kernels below their channel capacity class (4, 8,
+    # .., 32 and 18): channel counts between the classes, odd ones included,
+    # for the forward (C), the input gradient (K) and the weight gradient
+    "f32_c3": Layer("f32_c3", 2, 3, 12, 34, 30, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 109),
+    "f32_c13": Layer("f32_c13", 2, 13, 20, 40, 36, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 110),
+    "f32_c17": Layer("f32_c17", 1, 17, 30, 48, 40, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 111),
+    "f32_c29": Layer("f32_c29", 1, 29, 7, 36, 36, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 112),
+    "k1_c22_f32": Layer("k1_c22_f32", 2, 22, 11, 24, 20, 1, 1, 1, 0, 2, 2, 0, "f32", "uniform", 113),
 }
 
 
@@ -171,7 +179,8 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
                                   "k80_bf16", "c48k64_bf16", "s2dec_bf16", "s2k7dec_f32", "taps5_bf16", "s2taps_bf16",
                                   "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16", "bp7_bf16", "bp3_bf16",
                                   "roll_bf16", "roll96_bf16", "roll5_bf16", "roll5b_bf16",
-                                  "roll50_bf16", "roll5c_bf16", "roll5d_bf16", "roll5e_bf16"])
+                                  "roll50_bf16", "roll5c_bf16", "roll5d_bf16", "roll5e_bf16",
+                                  "f32_c3", "f32_c17", "k1_c22_f32"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
