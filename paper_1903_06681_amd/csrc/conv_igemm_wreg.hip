@@ -32,7 +32,22 @@ __device__ __forceinline__ void wreg_store(float* p, float v) {
     asm volatile("global_store_dword %0, %1, off sc1" : : "v"(p), "a"(v) : "memory");
 }
 
+// The same through a buffer resource over the workgroup's output block, for
+// the stores of interior blocks: the channel's offset oc * cstride (bytes)
+// is formed by the scalar unit inside the statement (OC is a compile-time
+// channel), added to the row's offset; the lane's part is voff.  Written as
+// a 64-bit address expression, the per-channel offsets stayed live, ran the
+// kernel out of scalar registers and were read back from lanes of a vector
+// register (v_readlane) in front of every store.
+template <int OC>
+__device__ __forceinline__ void wreg_store_oc(__amdgpu_buffer_rsrc_t rs, int voff, int rowoff, int cstride, float v) {
+    int so;
+    asm volatile("s_mul_i32 %0, %1, %2\n\ts_add_i32 %0, %0, %3\n\tbuffer_store_dword %4, %5, %6, %0 offen sc1"
+                 : "=&s"(so) : "s"(cstride), "n"(OC), "s"(rowoff), "a"(v), "v"(voff), "s"(rs));
+}
+
 static constexpr int kWThreads = 256;
+static constexpr int kWWord3 = 0x00020000;   // buffer resource word 3 (gfx9 family: raw dword access)
 
 // 8x8 transpose of 16-bit elements: in[c] holds 8 pixels of channel c,
 // out[p] receives the 8 channels of pixel p.
@@ -360,6 +375,14 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
     // output of this lane's pixel at channel o0 + 4*hi; channel o0 + 4*hi + c is c*oplane further
     float* const out = a.out + tile * a.out_tile + (int64_t(n) * a.Cout + o0 + 4 * hi) * oplane +
                        int64_t(v) * a.ostr + a.oph_c;
+    // the same as a buffer: base at channel o0, this lane's byte offset, and
+    // the byte strides of a channel and a row (the plan keeps the block below
+    // 2^31 bytes)
+    float* const outb = a.out + tile * a.out_tile + (int64_t(n) * a.Cout + o0) * oplane;
+    const __amdgpu_buffer_rsrc_t rout =
+        __builtin_amdgcn_make_buffer_rsrc(outb, 0, int((int64_t(a.Cout) - o0) * oplane * 4), kWWord3);
+    const int voff_out = int(((4 * hi) * oplane + int64_t(v) * a.ostr + a.oph_c) * 4);
+    const int opl4 = int(oplane * 4);
     // every lane's pixel and every channel of the block in range: stores need no masks
     const bool block_full = !BP && (MF || v0 + 64 <= a.Vo) && (o0 + OBT <= a.Cout);
     auto out_row = [&](int u) { return out + int64_t(u * a.ostr + a.oph_r) * a.out_cols; };
@@ -416,14 +439,19 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
         };
         const int u_prev = u0 + 2 * (i - 1) + wrow;
         const bool fast = i > 0 && block_full && u_prev < u_end;
-        float* const prow = out_row(u_prev);
+        // (uniform in the wave: u_prev's row term depends on the wave only)
+        const int prow4 = __builtin_amdgcn_readfirstlane(int(int64_t(u_prev * a.ostr + a.oph_r) * a.out_cols * 4));
         auto store_prev = [&](auto sc) {
             constexpr int s = decltype(sc)::value, sob = s / 16, e = s % 16;
             constexpr int oc = sob * 32 + 8 * (e / 4) + (e % 4);
+            // (operands through locals: this compiler does not capture
+            // variables that a lambda names only in asm operands)
+            const __amdgpu_buffer_rsrc_t rs = rout;
+            const int vo = voff_out, ro = prow4, cs = opl4;
             if constexpr (MF) {
-                if (v < a.Vo) wreg_store(prow + int64_t(oc) * oplane, prev[sob][e]);
+                if (v < a.Vo) wreg_store_oc<oc>(rs, vo, ro, cs, prev[sob][e]);
             } else {
-                wreg_store(prow + int64_t(oc) * oplane, prev[sob][e]);
+                wreg_store_oc<oc>(rs, vo, ro, cs, prev[sob][e]);
             }
         };
         auto mfmas = [&](auto with_stores) {
@@ -566,6 +594,8 @@ bool igemm_wreg_plan(IgemmArgs& a) {
                      : int((int64_t(a.Cin) * T) % 8 == 0);
     const int lds = wreg_lds(NOB, a.Tr, a.Ts, CG);
     if (lds > device_lds_limit()) return false;
+    // interior stores address a sample's output channels with 32-bit byte offsets
+    if (int64_t(a.Cout) * a.out_rows * a.out_cols * 4 >= (int64_t(1) << 31)) return false;
     a.OB = NOB * 32;
     wreg_segments(a);
     a.lds_bytes = lds;
