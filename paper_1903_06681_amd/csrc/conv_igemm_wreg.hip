@@ -59,8 +59,8 @@ __device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[
 #pragma unroll
         for (int j = 0; j < 4; ++j) {  // channel pair (2j, 2j+1)
             const uint32_t lo = s[(2 * j) * 4 + m], hi = s[(2 * j + 1) * 4 + m];
-            d[(2 * m) * 4 + j] = (lo & 0xffffu) | (hi << 16);
-            d[(2 * m + 1) * 4 + j] = (lo >> 16) | (hi & 0xffff0000u);
+            d[(2 * m) * 4 + j] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);      // low halves
+            d[(2 * m + 1) * 4 + j] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);  // high halves
         }
 }
 
@@ -338,9 +338,9 @@ __global__ __launch_bounds__(kWThreads, MINWG) void igemm_wreg_kernel(IgemmArgs 
             static_for<0, 4>([&](auto qc) {
                 constexpr int q = decltype(qc)::value;
                 constexpr int e0 = (2 * q) * T + t, e1 = (2 * q + 1) * T + t;
-                const uint32_t lo = (e0 & 1) ? (seg[e0 >> 1] >> 16) : (seg[e0 >> 1] & 0xffffu);
-                const uint32_t hi16 = (e1 & 1) ? (seg[e1 >> 1] & 0xffff0000u) : (seg[e1 >> 1] << 16);
-                p.d[q] = lo | hi16;
+                // element e0 into the low half, e1 into the high half: one byte permute
+                constexpr uint32_t sel = ((e0 & 1) ? 0x0302u : 0x0100u) | (((e1 & 1) ? 0x0706u : 0x0504u) << 16);
+                p.d[q] = __builtin_amdgcn_perm(seg[e1 >> 1], seg[e0 >> 1], sel);
             });
             Wf[ob][t * CG + cg] = p.b;
         });
