@@ -128,6 +128,10 @@ SMALL = {
     "f32_c17": Layer("f32_c17", 1, 17, 30, 48, 40, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 111),
     "f32_c29": Layer("f32_c29", 1, 29, 7, 36, 36, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 112),
     "k1_c22_f32": Layer("k1_c22_f32", 2, 22, 11, 24, 20, 1, 1, 1, 0, 2, 2, 0, "f32", "uniform", 113),
+    # the ends of the classes: one channel (class 4), and 36 / 40 channels,
+    # past the largest class, on the chunked and row kernels instead
+    "f32_c1": Layer("f32_c1", 2, 1, 3, 20, 24, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 114),
+    "f32_c36": Layer("f32_c36", 1, 36, 40, 24, 24, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 115),
 }
 
 
@@ -180,7 +184,7 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
                                   "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16", "bp7_bf16", "bp3_bf16",
                                   "roll_bf16", "roll96_bf16", "roll5_bf16", "roll5b_bf16",
                                   "roll50_bf16", "roll5c_bf16", "roll5d_bf16", "roll5e_bf16",
-                                  "f32_c3", "f32_c17", "k1_c22_f32"])
+                                  "f32_c3", "f32_c17", "k1_c22_f32", "f32_c1", "f32_c36"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
