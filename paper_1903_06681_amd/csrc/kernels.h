@@ -76,7 +76,7 @@ struct IgemmArgs {
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
     int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32);
-                                 // 3: register-weight rolling-row kernel (bf16)
+                                 // 3: register-weight rolling-row kernel (bf16); 4: frame kernel (bf16)
     int phase;                   // register-weight bf16 forward over the stride-2 phase images
     // merged-phase backward-data (stride 2, C <= 8): all four output phases
     // as one stride-1 correlation over dy; rows o' = 4 c + 2 py + px of the
@@ -87,9 +87,10 @@ struct IgemmArgs {
     int bp, bpC, bpvoff;
     int bpdr[2], bptr[2], bpr0[2], bpdc[2], bpts[2], bps0[2];
     int nvb, nseg, rows_per_seg; // strip kernels: 64- (128-, rolling) column strips, row segments
-    // frame mode (chunked kernels only): the launch covers only the output
-    // rectangles [fu0, fu0 + fnu) x [fv0, fv0 + fnv) of fseg segments, whose
-    // workgroups are numbered from fblk[seg] (prefix sums, fblk[fseg] total)
+    // frame mode (chunked and frame kernels): the launch covers only the
+    // output rectangles [fu0, fu0 + fnu) x [fv0, fv0 + fnv) of fseg segments,
+    // whose workgroups are numbered from fblk[seg] (prefix sums, fblk[fseg]
+    // total; the plan sets them for the kernel it picks)
     int frame, fseg;
     int fu0[4], fv0[4], fnu[4], fnv[4], fcm[4], fblk[5];
 };
@@ -111,6 +112,8 @@ bool igemm_roll_plan(IgemmArgs& a);
 hipError_t launch_igemm_roll(const IgemmArgs& a, hipStream_t s);
 bool igemm_f32w_plan(IgemmArgs& a);
 hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s);
+bool igemm_frame_plan(IgemmArgs& a);
+hipError_t launch_igemm_frame(const IgemmArgs& a, hipStream_t s);
 
 // ----------------------------------------------------- weight gradient
 //

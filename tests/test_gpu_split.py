@@ -44,6 +44,10 @@ LAYERS = {
     "f32": wl.small("c4", H=96, W=80, P=3, Q=2),
     "odd": Layer("odd", 2, 5, 7, 26, 39, 3, 3, 1, 1, 2, 3, 2, "bf16", "uniform", 203),
     "odd32": Layer("odd32", 2, 5, 7, 26, 39, 3, 3, 1, 1, 2, 3, 2, "f32", "uniform", 204),
+    # frame kernel: two channel chunks (96 = 64 + 32 of 64), 40 output
+    # channels (a partial 32-channel block); 7x7 (bands three wide, 98 groups)
+    "wide": Layer("wide", 2, 96, 40, 64, 80, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 205),
+    "k7": Layer("k7", 1, 16, 24, 48, 72, 7, 7, 1, 3, 2, 2, 3, "bf16", "uniform", 206),
 }
 
 
