@@ -48,6 +48,10 @@ LAYERS = {
     # channels (a partial 32-channel block); 7x7 (bands three wide, 98 groups)
     "wide": Layer("wide", 2, 96, 40, 64, 80, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 205),
     "k7": Layer("k7", 1, 16, 24, 48, 72, 7, 7, 1, 3, 2, 2, 3, "bf16", "uniform", 206),
+    # frame kernel: 24 channels (a 3-group chunk: the runtime instantiation);
+    # 128 -> 64 channels (whole chunks, weights copied raw, two chunks)
+    "c24": Layer("c24", 2, 24, 32, 40, 56, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 207),
+    "deep": Layer("deep", 2, 128, 64, 48, 64, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 208),
 }
 
 
