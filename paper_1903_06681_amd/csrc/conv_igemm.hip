@@ -351,9 +351,9 @@ bool igemm_plan(IgemmArgs& a, int dtype) {
     a.kind = 0;
     // a merged-phase backward-data request runs on the register-weight kernel or not at all
     if (a.bp) return dtype == 1 && igemm_wreg_plan(a);
-    // a frame runs on the frame kernel (bf16) or the chunked kernel (the strip
+    // a frame runs on the frame kernel, else on the chunked kernel (the strip
     // kernels cover whole tiles)
-    if (a.frame && dtype == 1 && igemm_frame_plan(a)) return true;
+    if (a.frame && igemm_frame_plan(a, dtype)) return true;
     if (!a.frame) {
         if (dtype == 1 && igemm_roll_plan(a)) return true;
         if (dtype == 1 && igemm_wreg_plan(a)) return true;
@@ -388,7 +388,7 @@ hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
     if (a.kind == 1) return launch_igemm_wreg(a, s);
     if (a.kind == 2) return launch_igemm_f32w(a, s);
     if (a.kind == 3) return launch_igemm_roll(a, s);
-    if (a.kind == 4) return launch_igemm_frame(a, s);
+    if (a.kind == 4) return launch_igemm_frame(a, dtype, s);
     const int nvb = (a.Vo + kBW - 1) / kBW, nub = (a.Uo + kBH - 1) / kBH;
     dim3 grid(a.frame ? a.fblk[a.fseg] : nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
     if (grid.x == 0) return hipSuccess;   // an empty frame

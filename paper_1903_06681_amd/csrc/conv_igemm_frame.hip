@@ -1,17 +1,17 @@
-// Boundary frame of a tile, bf16 (the outputs of Eqs. (1) / (3) whose window
-// reads a halo margin; Sec. IV-A computes them after the exchange, the
-// interior before it).
+// Boundary frame of a tile, bf16 and fp32 (the outputs of Eqs. (1) / (3)
+// whose window reads a halo margin; Sec. IV-A computes them after the
+// exchange, the interior before it).
 //
 // The frame is a few output lines (the rows of the top and bottom bands, the
 // columns of the left and right bands), each one output pixel wide.  A
 // workgroup computes 32 consecutive outputs of one line for 32 output
 // channels: one 32x32 MFMA tile, D[o][pixel] = sum_kg A[o][kg] B[kg][pixel]
-// with kg = (tap, input channel) as in the whole-tile kernels.  The four
-// waves split the reduction over kg (k-steps w, w+4, ...) and sum their tiles
-// through LDS, so that a frame of ~1,000 pixels per image and 64 channels
-// still spreads over a few hundred workgroups.
+// with kg = (tap, input channel) as in the whole-tile kernels.  Its waves
+// (four for bf16, eight for fp32) split the reduction over kg and sum their
+// tiles through LDS, so that a frame of ~1,000 pixels per image and 64
+// channels still spreads over a few hundred workgroups.
 //
-// Per channel chunk the weights of the block ([o][tap, 8-channel group][8])
+// bf16: per channel chunk the weights of the block ([o][tap, 8-channel group][8])
 // and the input window of the line piece (along x across x channels,
 // channel-innermost) are gathered from NCHW with 2-byte buffer loads: an
 // element outside the tensors (padding channels, rows or columns past the
@@ -34,6 +34,16 @@ constexpr int kPiece = 32;   // outputs of a line per workgroup (MFMA columns)
 constexpr int kOB = 32;      // output channels per workgroup (MFMA rows)
 constexpr int kWB = 9;       // weight items (8 loads each) per thread per batch
 constexpr int kPB = 4;       // window items per thread per batch
+// fp32: eight waves (two per SIMD: a frame of a small layer is few
+// workgroups, whose staging is VALU work), and the elements per thread and
+// batch of the weights and the window
+constexpr int kWavesF = 8, kThreadsF = 64 * kWavesF;
+constexpr int kWF = 20;
+constexpr int kPF = 8;
+// fp32 weight row stride (floats): one more than the 32 output channels, so
+// that the stores of items along a weight row (different k, one channel)
+// fall in different banks
+constexpr int kWS = kOB + 1;
 constexpr int kWord3 = 0x00020000;   // buffer resource word 3 (gfx9 family: raw access)
 constexpr int kOOB = 0x7fffffff;     // byte offset past every buffer here: the load returns 0
 typedef unsigned f_v4u __attribute__((ext_vector_type(4)));
@@ -54,6 +64,13 @@ __host__ __device__ inline int frame_wl_elems(int Tt, int CC) {
     return (m + 7) / 8 * 8;
 }
 
+// fp32: weights [Tt * CC][kWS] and the larger window [CC][PA][TA] floats
+int frame_lds_f32(const IgemmArgs& a, int CC) {
+    const int Tt = a.Tr * a.Ts;
+    const int win = std::max((kPiece - 1 + a.Ts) * a.Tr, (kPiece - 1 + a.Tr) * a.Ts) * CC;
+    return std::max((Tt * CC * kWS + win) * 4, kWavesF * 4 * 1024);
+}
+
 int frame_lds(const IgemmArgs& a, int CC) {
     // window of a row line, of a column line: (along) x (across) pixels
     const int win = std::max((kPiece - 1 + a.Ts) * a.Tr, (kPiece - 1 + a.Tr) * a.Ts) * frame_ps(CC) * 2;
@@ -62,6 +79,75 @@ int frame_lds(const IgemmArgs& a, int CC) {
 }
 
 }  // namespace
+
+// Sums the NWV waves' tiles through LDS (red[wave][value i][lane], NWV * 4
+// KB at the start of the workgroup's LDS, after a barrier) and stores the
+// piece: thread (q = wave, lane) sums values i = q + NWV m, which are
+// output channel 8 (i / 4) + 4 (lane / 32) + i % 4, pixel lane % 32 of the
+// tile (MFMA D layout), in the order of the waves.
+template <int NWV>
+__device__ __forceinline__ void frame_sum_store(const IgemmArgs& a, const floatx16& acc, unsigned char* smem,
+                                                int tile, int n, int o0, bool cm, int u, int v, int n_out) {
+    static_assert(NWV == 4 || NWV == 8, "four or eight waves");
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int l32 = lane & 31, hi = lane >> 5;
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) red[(wave * 16 + i) * 64 + lane] = acc[i];
+    __syncthreads();
+    float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
+    if (l32 < n_out) {
+        const int pu = cm ? u + l32 : u, pv = cm ? v : v + l32;
+        const int orow = pu * a.ostr + a.oph_r, ocol = pv * a.ostr + a.oph_c;
+#pragma unroll
+        for (int m = 0; m < 16 / NWV; ++m) {
+            const int i = wave + NWV * m;
+            float s = red[i * 64 + lane];
+#pragma unroll
+            for (int w = 1; w < NWV; ++w) s += red[(w * 16 + i) * 64 + lane];
+            const int o = o0 + 8 * (i / 4) + 4 * hi + i % 4;
+            if (o < a.Cout) out[(int64_t(o) * a.out_rows + orow) * a.out_cols + ocol] = s;
+        }
+    }
+}
+
+// n / d and n % d (0 <= n < 2^22, d >= 1) from a float reciprocal of d: the
+// product is within one of the quotient, which one correction each way
+// makes exact.
+__device__ __forceinline__ int frame_divmod(int n, int d, float inv, int& r) {
+    int q = int(float(n) * inv);
+    r = n - q * d;
+    const bool lo = r < 0;
+    q -= lo ? 1 : 0;
+    r += lo ? d : 0;
+    const bool hi = r >= d;
+    q += hi ? 1 : 0;
+    r -= hi ? d : 0;
+    return q;
+}
+
+// Segment, line and piece of this workgroup: the line's first output pixel
+// (u, v), whether it is a column of the side bands (cm), outputs in the piece.
+struct FramePiece {
+    int u, v, n_out;
+    bool cm;
+};
+
+__device__ __forceinline__ FramePiece frame_piece(const IgemmArgs& a) {
+    int sg = 0;
+    while (sg + 1 < a.fseg && int(blockIdx.x) >= a.fblk[sg + 1]) ++sg;
+    FramePiece f;
+    f.cm = a.fcm[sg] != 0;
+    const int len = f.cm ? a.fnu[sg] : a.fnv[sg];
+    const int npc = (len + kPiece - 1) / kPiece;
+    const int local = blockIdx.x - a.fblk[sg];
+    const int line = local / npc, p0 = (local - line * npc) * kPiece;
+    f.n_out = min(kPiece, len - p0);
+    f.u = a.fu0[sg] + (f.cm ? p0 : line);
+    f.v = a.fv0[sg] + (f.cm ? line : p0);
+    return f;
+}
 
 // TR, TS: filter taps (rows, columns) of the launch; CCG: 8-channel groups
 // per chunk.  Non-zero values make every index division one by a constant
@@ -78,19 +164,9 @@ __global__ __launch_bounds__(kThreads) void igemm_frame_bf16_kernel(IgemmArgs a)
     extern __shared__ __align__(16) unsigned char smem[];
     const int Tr = TR > 0 ? TR : a.Tr, Ts = TS > 0 ? TS : a.Ts;
     const int CCG = CCG_ > 0 ? CCG_ : a.CC / 8, CC = CCG * 8;
-    // segment, line and piece of this workgroup
-    int sg = 0;
-    while (sg + 1 < a.fseg && int(blockIdx.x) >= a.fblk[sg + 1]) ++sg;
-    const bool cm = a.fcm[sg] != 0;   // a column of the left / right band
-    const int len = cm ? a.fnu[sg] : a.fnv[sg];
-    const int npc = (len + kPiece - 1) / kPiece;
-    const int local = blockIdx.x - a.fblk[sg];
-    const int line = local / npc, p0 = (local - line * npc) * kPiece;
-    const int n_out = min(kPiece, len - p0);
-    // first output pixel (u, v) of the piece; the line runs along v (rows of
-    // the frame) or along u (columns)
-    const int u = a.fu0[sg] + (cm ? p0 : line);
-    const int v = a.fv0[sg] + (cm ? line : p0);
+    const FramePiece fp = frame_piece(a);
+    const bool cm = fp.cm;   // a column of the left / right band
+    const int u = fp.u, v = fp.v, n_out = fp.n_out;
 
     // window extent along the line and across it
     const int PA = (kPiece - 1) + (cm ? Tr : Ts), TA = cm ? Ts : Tr;
@@ -253,43 +329,154 @@ __global__ __launch_bounds__(kThreads) void igemm_frame_bf16_kernel(IgemmArgs a)
         }
     }
 
-    // sum the four waves' tiles: red[wave][value i][lane]
-    __syncthreads();
-    float* red = reinterpret_cast<float*>(smem);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) red[(wave * 16 + i) * 64 + lane] = acc[i];
-    __syncthreads();
-    // thread (q = wave, lane) sums values i = q + 4 m: output channel
-    // 8 m + 4 (lane / 32) + q, pixel lane % 32 (MFMA D layout)
-    float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
-    if (l32 < n_out) {
-        const int pu = cm ? u + l32 : u, pv = cm ? v : v + l32;
-        const int orow = pu * a.ostr + a.oph_r, ocol = pv * a.ostr + a.oph_c;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const int i = wave + 4 * m;
-            const float s = red[(0 * 16 + i) * 64 + lane] + red[(1 * 16 + i) * 64 + lane] +
-                            red[(2 * 16 + i) * 64 + lane] + red[(3 * 16 + i) * 64 + lane];
-            const int o = o0 + 8 * m + 4 * hi + wave;
-            if (o < a.Cout) out[(int64_t(o) * a.out_rows + orow) * a.out_cols + ocol] = s;
-        }
-    }
+    frame_sum_store<4>(a, acc, smem, tile, n, o0, cm, u, v, n_out);
 }
 
-bool igemm_frame_plan(IgemmArgs& a) {
+// fp32: v_mfma_f32_32x32x2_f32 (eight waves splitting the reduction), a
+// k-step is one (tap, input channel) per half-wave: lanes 0-31 channel 2 c2, lanes 32-63 channel 2 c2 + 1 of one
+// tap.  Per chunk of CC channels (even) the weights lie in LDS as
+// [tap * CC + ci][32 output channels, padded to 33] and the window as
+// [ci][along][across] floats; both are read one float per lane.  Weight items are
+// taken in the tensor's own order (a row of the [K][C][R][S] tensor: taps
+// and input channels of one output channel forward, taps and output
+// channels of one input channel for the input gradient), so the loads are
+// contiguous; the tap flip of Eq. (3) is applied when they are placed.
+template <int TR, int TS>
+__global__ __launch_bounds__(kThreadsF) void igemm_frame_f32_kernel(IgemmArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int Tr = TR > 0 ? TR : a.Tr, Ts = TS > 0 ? TS : a.Ts, Tt = Tr * Ts;
+    const int CC = a.CC, CCH = CC / 2;
+    const FramePiece fp = frame_piece(a);
+    const bool cm = fp.cm;
+    const int u = fp.u, v = fp.v, n_out = fp.n_out;
+    const int PA = (kPiece - 1) + (cm ? Tr : Ts), TA = cm ? Ts : Tr;
+    float* wl = reinterpret_cast<float*>(smem);   // [Tt * CC][kWS]
+    float* pl = wl + Tt * CC * kWS;               // [CC][PA][TA]
+
+    const int o0 = blockIdx.y * kOB;
+    const int tile = blockIdx.z / a.Nn, n = blockIdx.z % a.Nn;
+    const int64_t plane = int64_t(a.in_rows) * a.in_pitch;
+    const float* in = static_cast<const float*>(a.in) + tile * a.in_tile + int64_t(n) * a.Cin * plane;
+    const __amdgpu_buffer_rsrc_t rin =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(in), 0, int(a.Cin * plane * 4), kWord3);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(a.w), 0, a.wK * a.wC * a.R * a.S * 4, kWord3);
+    const int w_os = int(a.w_os), w_cs = int(a.w_cs), iplane = int(plane);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int row0 = u + a.base_r, col0 = v + a.base_c;   // window origin (stride 1)
+
+    floatx16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+
+    // weight rows: forward, output channel ol with CC * Tt elements (ci, tap);
+    // input gradient, input channel ci with kOB * Tt elements (o, tap)
+    const int rowlen = (a.wmode ? kOB : CC) * Tt, nw = (a.wmode ? CC : kOB) * rowlen;
+    const float rinv = 1.0f / float(rowlen);
+    const int np = CC * PA * TA;
+    for (int c0 = 0; c0 < a.Cin; c0 += CC) {
+        __syncthreads();
+        // one batch of weight and one of window elements per pass, all loads
+        // of the pass issued before its first store
+        const int nbw = (nw + kThreadsF * kWF - 1) / (kThreadsF * kWF);
+        const int nbp = (np + kThreadsF * kPF - 1) / (kThreadsF * kPF);
+        for (int b = 0; b < nbw || b < nbp; ++b) {
+            float wv[kWF], pv[kPF];
+            int ws_[kWF], ps_[kPF];
+            if (b < nbw) {
+                const int e0 = tid + b * kThreadsF * kWF;
+#pragma unroll
+                for (int q = 0; q < kWF; ++q) {
+                    const int e = e0 + q * kThreadsF;
+                    const int ec = min(e, nw - 1);
+                    int rem;
+                    const int row = frame_divmod(ec, rowlen, rinv, rem);
+                    const int x = rem / Tt, rt = rem - x * Tt;   // channel within the row, raw tap
+                    const int ol = a.wmode ? x : row, ci = a.wmode ? row : x;
+                    const int wr = rt / Ts, wsc = rt - wr * Ts;   // stride 1: the filter is Tr x Ts
+                    // kernel tap (tr, ts) of filter tap (wr, wsc): wr = wr0 + wrstep tr, wrstep = +-1
+                    const int t = (wr - a.wr0) * a.wrstep * Ts + (wsc - a.ws0) * a.wsstep;
+                    const int o = o0 + ol, cg = c0 + ci;
+                    const int off = (o < a.Cout && cg < a.Cin) ? 4 * (o * w_os + cg * w_cs + rt) : kOOB;
+                    wv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, off, 0, 0));
+                    ws_[q] = e < nw ? (t * CC + ci) * kWS + ol : -1;
+                }
+            }
+            if (b < nbp) {
+                // window: item (channel, along, across), the input column fastest
+                const int e0 = tid + b * kThreadsF * kPF;
+#pragma unroll
+                for (int q = 0; q < kPF; ++q) {
+                    const int e = e0 + q * kThreadsF;
+                    const int ec = min(e, np - 1);
+                    int al, ac, ci;
+                    if (!cm) { al = ec % PA; const int r = ec / PA; ac = r % TA; ci = r / TA; }
+                    else { ac = ec % TA; const int r = ec / TA; al = r % PA; ci = r / PA; }
+                    const int gr = row0 + (cm ? al : ac), gc = col0 + (cm ? ac : al);
+                    const bool ok = gr >= 0 && gr < a.in_rows && gc >= 0 && gc < a.in_cols && c0 + ci < a.Cin;
+                    const int off = ok ? 4 * ((c0 + ci) * iplane + gr * a.in_pitch + gc) : kOOB;
+                    pv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rin, off, 0, 0));
+                    ps_[q] = e < np ? (ci * PA + al) * TA + ac : -1;
+                }
+            }
+            if (b < nbw) {
+#pragma unroll
+                for (int q = 0; q < kWF; ++q)
+                    if (ws_[q] >= 0) wl[ws_[q]] = wv[q];
+            }
+            if (b < nbp) {
+#pragma unroll
+                for (int q = 0; q < kPF; ++q)
+                    if (ps_[q] >= 0) pl[ps_[q]] = pv[q];
+            }
+        }
+        __syncthreads();
+
+        // k-steps (tap t, channel pair c2), t-major; wave w takes the
+        // contiguous eighth [w nk / 8, (w + 1) nk / 8)
+        const int nk = Tt * CCH;
+        const int kb = wave * nk / kWavesF, ke = (wave + 1) * nk / kWavesF;
+        int t = kb / CCH, c2 = kb - t * CCH;
+        auto kstep = [&]() __attribute__((always_inline)) {
+            const int ci = 2 * c2 + hi;
+            const int tr = t / Ts, ts = t - tr * Ts;
+            const float A = wl[(t * CC + ci) * kWS + l32];
+            const int al = l32 + (cm ? tr : ts), ac = cm ? ts : tr;
+            const float B = pl[(ci * PA + al) * TA + ac];
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(A, B, acc, 0, 0, 0);
+            const bool wrap = ++c2 == CCH;
+            c2 = wrap ? 0 : c2;
+            t += wrap ? 1 : 0;
+        };
+        // four steps per pass: their operand reads can be issued ahead of
+        // the MFMAs
+        int kk = kb;
+        for (; kk + 4 <= ke; kk += 4) { kstep(); kstep(); kstep(); kstep(); }
+        for (; kk < ke; ++kk) kstep();
+    }
+    frame_sum_store<kWavesF>(a, acc, smem, tile, n, o0, cm, u, v, n_out);
+}
+
+bool igemm_frame_plan(IgemmArgs& a, int dtype) {
     if (!a.frame || a.istr != 1 || a.Tr * a.Ts == 0 || a.bp) return false;
+    // the tap flip is read back as (wr - wr0) * wrstep: unit tap steps only
+    if ((a.wrstep != 1 && a.wrstep != -1) || (a.wsstep != 1 && a.wsstep != -1)) return false;
     // byte offsets of the buffer loads are 32-bit
-    if (int64_t(a.Cin) * a.in_rows * a.in_pitch * 2 >= kOOB ||
-        int64_t(a.wK) * a.wC * a.R * a.S * 2 >= kOOB)
+    const int es = dtype == 1 ? 2 : 4;
+    if (int64_t(a.Cin) * a.in_rows * a.in_pitch * es >= kOOB || int64_t(a.wK) * a.wC * a.R * a.S * es >= kOOB)
         return false;
-    const int cin_r = (a.Cin + 7) / 8 * 8;
+    // channel chunks, widest first: bf16 multiples of 8 up to 64, fp32 even up to 32
+    const int gran = dtype == 1 ? 8 : 2, maxcc = dtype == 1 ? 64 : 32;
+    const int cin_r = (a.Cin + gran - 1) / gran * gran;
+    int cands[8], nc = 0;
+    cands[nc++] = std::min(cin_r, maxcc);
+    for (int c = maxcc; c >= gran; c /= 2)
+        if (c < cands[0]) cands[nc++] = c;
     const int limit = device_lds_limit();
-    int cands[4] = {std::min(cin_r, 64), 32, 16, 8}, nc = 0;
-    for (int i = 0; i < 4; ++i)
-        if (i == 0 || cands[i] < cands[0]) cands[nc++] = cands[i];
     for (int budget : {std::min(80 * 1024, limit), limit}) {
         for (int i = 0; i < nc; ++i) {
-            const int b = frame_lds(a, cands[i]);
+            const int b = dtype == 1 ? frame_lds(a, cands[i]) : frame_lds_f32(a, cands[i]);
             if (b <= budget) {
                 a.CC = cands[i];
                 a.lds_bytes = b;
@@ -338,9 +525,24 @@ static hipError_t launch_frame_taps(const IgemmArgs& a, dim3 grid, hipStream_t s
     }
 }
 
-hipError_t launch_igemm_frame(const IgemmArgs& a, hipStream_t s) {
+template <int TR, int TS>
+static hipError_t launch_frame_f32(const IgemmArgs& a, dim3 grid, hipStream_t s) {
+    const void* f = reinterpret_cast<const void*>(igemm_frame_f32_kernel<TR, TS>);
+    if (a.lds_bytes > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((igemm_frame_f32_kernel<TR, TS>), grid, dim3(kThreadsF), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_igemm_frame(const IgemmArgs& a, int dtype, hipStream_t s) {
     dim3 grid(a.fblk[a.fseg], (a.Cout + kOB - 1) / kOB, a.ntiles * a.Nn);
     if (grid.x == 0) return hipSuccess;   // an empty frame
+    if (dtype != 1) {
+        if (a.Tr == 3 && a.Ts == 3) return launch_frame_f32<3, 3>(a, grid, s);
+        return launch_frame_f32<0, 0>(a, grid, s);
+    }
     if (a.Tr == 3 && a.Ts == 3) return launch_frame_taps<3>(a, grid, s);
     if (a.Tr == 5 && a.Ts == 5) return launch_frame_taps<5>(a, grid, s);
     if (a.Tr == 7 && a.Ts == 7) return launch_frame_taps<7>(a, grid, s);

@@ -76,7 +76,7 @@ struct IgemmArgs {
     int OB;                      // output channels per workgroup (32 or 64)
     int lds_bytes;
     int kind;                    // 0: chunked kernel; 1, 2: register-weight strip kernel (bf16, fp32);
-                                 // 3: register-weight rolling-row kernel (bf16); 4: frame kernel (bf16)
+                                 // 3: register-weight rolling-row kernel (bf16); 4: frame kernel (bf16, fp32)
     int phase;                   // register-weight bf16 forward over the stride-2 phase images
     // merged-phase backward-data (stride 2, C <= 8): all four output phases
     // as one stride-1 correlation over dy; rows o' = 4 c + 2 py + px of the
@@ -112,8 +112,8 @@ bool igemm_roll_plan(IgemmArgs& a);
 hipError_t launch_igemm_roll(const IgemmArgs& a, hipStream_t s);
 bool igemm_f32w_plan(IgemmArgs& a);
 hipError_t launch_igemm_f32w(const IgemmArgs& a, hipStream_t s);
-bool igemm_frame_plan(IgemmArgs& a);
-hipError_t launch_igemm_frame(const IgemmArgs& a, hipStream_t s);
+bool igemm_frame_plan(IgemmArgs& a, int dtype);
+hipError_t launch_igemm_frame(const IgemmArgs& a, int dtype, hipStream_t s);
 
 // ----------------------------------------------------- weight gradient
 //

@@ -52,6 +52,9 @@ LAYERS = {
     # 128 -> 64 channels (whole chunks, weights copied raw, two chunks)
     "c24": Layer("c24", 2, 24, 32, 40, 56, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 207),
     "deep": Layer("deep", 2, 128, 64, 48, 64, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 208),
+    # fp32 frame kernel: 5x5 (the runtime instantiation), 40 channels in
+    # chunks of 16 (the last one partial), 24 output channels
+    "f32k5": Layer("f32k5", 1, 40, 24, 40, 48, 5, 5, 1, 2, 2, 2, 2, "f32", "uniform", 209),
 }
 
 
