@@ -10,7 +10,9 @@ not reach on their own:
   bit-identical to the run with real margins (it reads no dy halo, Sec.
   III-A) and to a second run (fixed-order reduction);
 * the benchmark's two-stream step (the dy halo exchange beside the weight
-  gradient, Sec. IV-A) equals the one-stream step bit for bit.
+  gradient, Sec. IV-A) equals the one-stream step bit for bit;
+* the interior / boundary split (Sec. IV-A) on the c5a, c5b and c4 tiles
+  equals the whole-tile passes bit for bit on integer-valued inputs.
 """
 import numpy as np
 import pytest
@@ -73,13 +75,13 @@ def test_halo_full_size_all_tiles_bit_exact(name, which):
         del win, got
 
 
-def _tile_setup(L, tile):
+def _tile_setup(L, tile, dist=None):
     """The benchmark's single-tile inputs: padded x and dy tiles with their
     halos filled through pack (all tiles) -> exchange -> unpack (this tile)."""
     p = dc.Problem.of(L)
     nt = L.P * L.Q
     tdt = H.TORCH_DT[L.dtype]
-    x, w, dy = wl.draw(L, "x"), wl.draw(L, "w"), wl.draw(L, "dy")
+    x, w, dy = wl.draw(L, "x", dist), wl.draw(L, "w", dist), wl.draw(L, "dy", dist)
     xt = H.alloc_tiles(p, X, nt, L.dtype)
     H.scatter_interiors(xt, H.to_device(x, L.dtype), p, X)
     sx = torch.empty((nt, dc.halo_elems(p, X)), dtype=tdt, device="cuda")
@@ -170,3 +172,36 @@ def test_two_stream_step_equals_one_stream_step():
             assert torch.equal(_bits(a), _bits(b)), (it, ("y", "dx", "dw", "send_x", "send_dy")[k])
     # the margins the second stream filled equal the one-stream ones
     assert torch.equal(_bits(dyp_nan), _bits(dyp))
+
+
+@pytest.mark.parametrize("name", ["c5a", "c5b", "c4"])
+def test_full_size_split_equals_whole_tile(name):
+    """The split step of the benchmark on an interior tile at full size (c5a:
+    the benchmark's; c5b: 5x5, bands two wide; c4: fp32): forward and input
+    gradient on the interior while every margin still holds NaN, then the
+    boundary frames once the margins are filled, equal the whole-tile passes
+    bit for bit.  Inputs are integers in [-2, 2]: every sum is exact in fp32,
+    so the frame kernels' order of additions and the whole-tile kernels' give
+    the same bits."""
+    L = wl.LAYERS[name]
+    tile = 5
+    print(f"[split full] {name} tile {tile}, integer inputs", flush=True)
+    p, wd, xp, dyp, dyp_nan, _, _ = _tile_setup(L, tile, dist="int")
+    h = L.halo
+    xp_nan = torch.full_like(xp, float("nan"))
+    xp_nan[..., h:h + L.Ht, h:h + L.Wt] = xp[..., h:h + L.Ht, h:h + L.Wt]
+    INT, BND = dc.DC_REGION_INTERIOR, dc.DC_REGION_BOUNDARY
+    y_ref = torch.empty((L.N, L.K, L.Hot, L.Wot), device="cuda")
+    dx_ref = torch.empty((L.N, L.C, L.Ht, L.Wt), device="cuda")
+    dc.conv_fwd(p, tile, xp, wd, y_ref)
+    dc.conv_bwd_data(p, tile, dyp, wd, dx_ref)
+    y = torch.full_like(y_ref, float("nan"))
+    dx = torch.full_like(dx_ref, float("nan"))
+    dc.conv_fwd_region(p, tile, INT, xp_nan, wd, y)
+    dc.conv_bwd_data_region(p, tile, INT, dyp_nan, wd, dx)
+    dc.conv_fwd_region(p, tile, BND, xp, wd, y)
+    dc.conv_bwd_data_region(p, tile, BND, dyp, wd, dx)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(y_ref).all()) and bool(torch.isfinite(dx_ref).all())
+    assert torch.equal(_bits(y), _bits(y_ref)), f"forward: {int((_bits(y) != _bits(y_ref)).sum())} mismatches"
+    assert torch.equal(_bits(dx), _bits(dx_ref)), f"input gradient: {int((_bits(dx) != _bits(dx_ref)).sum())} mismatches"
