@@ -32,6 +32,12 @@ namespace dc {
 static constexpr int kThreads = 256;
 static constexpr int kBH = 4;    // output rows per workgroup (one per wave)
 static constexpr int kBW = 64;   // output columns per workgroup (two 32-pixel MFMA tiles)
+// Staging batches: items per thread whose loads are all issued before the
+// first is waited for (bf16 items are 8 loads each; larger fp32 batches
+// measured slower)
+static constexpr int kUB = 4, kUF = 8;
+static constexpr int kRWord3c = 0x00020000;   // buffer resource word 3 (gfx9 family: raw access)
+static constexpr int kOOBc = 0x7fffffff;      // byte offset past every buffer here: the load returns 0
 
 // Pixel stride (bf16 elements) of the channel-innermost patch: an odd number
 // of 16-byte units, so 16 consecutive lanes reading 16 B each hit distinct
@@ -85,7 +91,11 @@ __device__ __forceinline__ void block_origin(const IgemmArgs& a, int& u0, int& v
     }
 }
 
-template <int OB>
+// RB: the sample's input and the weights are under 2^31 bytes, so the staging
+// gathers are buffer loads (an element outside the tensors is an offset past
+// the buffer's end, which reads zero): no branches, a thread's batch of loads
+// in flight together.  Otherwise the plain loop (one load round trip per item).
+template <int OB, bool RB>
 __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int NOB = OB / 32;
@@ -121,40 +131,94 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+    const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(in), 0, RB ? int(a.Cin * plane * 2) : 0, kRWord3c);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(w), 0, RB ? a.wK * a.wC * a.R * a.S * 2 : 0, kRWord3c);
     for (int c0 = 0; c0 < a.Cin; c0 += CC) {
         __syncthreads();
         // weights: one 8-channel vector per (group, output channel)
-        for (int e = tid; e < G * OB; e += kThreads) {
+        auto w_item = [&](int e, int j) -> int64_t {   // element offset of element j of item e, or -1
             const int g = e / OB, ol = e - g * OB;
             const int t = g / CCG, cb = g - t * CCG;
             const int tr = t / a.Ts, ts = t - tr * a.Ts;
-            const int o = o0 + ol;
+            const int o = o0 + ol, ci = c0 + cb * 8 + j;
             const int wr = a.wr0 + a.wrstep * tr, ws = a.ws0 + a.wsstep * ts;
-            Pack8 p;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int ci = c0 + cb * 8 + j;
-                p.h[j] = (o < a.Cout && ci < a.Cin)
-                             ? w[o * a.w_os + ci * a.w_cs + wr * a.S + ws]
-                             : uint16_t(0);
-            }
-            *reinterpret_cast<uint4*>(wl + e * 8) = p.v;
-        }
+            return (o < a.Cout && ci < a.Cin) ? o * a.w_os + ci * a.w_cs + wr * a.S + ws : -1;
+        };
         // input patch, transposed to channel-innermost
-        for (int e = tid; e < PR * CCG * PC; e += kThreads) {
+        auto p_item = [&](int e, int64_t& pix, int& cbase, int& slot) {   // pix < 0: outside the tile
             const int pc = e % PC;
             const int rest = e / PC;
             const int cg = rest % CCG, pr = rest / CCG;
             const int gr = row_in0 + pr, gc = col_in0 + pc;
             const bool ok = gr >= 0 && gr < a.in_rows && gc >= 0 && gc < a.in_cols;
-            const uint16_t* src = in + int64_t(gr) * a.in_pitch + gc;
-            Pack8 p;
+            pix = ok ? int64_t(gr) * a.in_pitch + gc : -1;
+            cbase = c0 + cg * 8;
+            slot = (pr * PC + pc) * PS + cg * 8;
+        };
+        if constexpr (RB) {
+            const int nw = G * OB, np = PR * CCG * PC;
+            for (int e0 = tid; e0 < nw; e0 += kThreads * kUB) {
+                Pack8 v[kUB];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int ci = c0 + cg * 8 + j;
-                p.h[j] = (ok && ci < a.Cin) ? src[int64_t(ci) * plane] : uint16_t(0);
+                for (int q = 0; q < kUB; ++q) {
+                    const int e = e0 + q * kThreads;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        // past the end: an out-of-range load, no memory access
+                        const int64_t off = e < nw ? w_item(e, j) : -1;
+                        v[q].h[j] = __builtin_amdgcn_raw_buffer_load_b16(rw, off >= 0 ? 2 * int(off) : kOOBc, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < kUB; ++q)
+                    if (e0 + q * kThreads < nw) *reinterpret_cast<uint4*>(wl + (e0 + q * kThreads) * 8) = v[q].v;
             }
-            *reinterpret_cast<uint4*>(pl + (pr * PC + pc) * PS + cg * 8) = p.v;
+            for (int e0 = tid; e0 < np; e0 += kThreads * kUB) {
+                Pack8 v[kUB];
+                int slot[kUB];
+#pragma unroll
+                for (int q = 0; q < kUB; ++q) {
+                    const int e = e0 + q * kThreads;
+                    int64_t pix = -1;   // past the end: out-of-range loads
+                    int cbase = 0;
+                    slot[q] = -1;
+                    if (e < np) p_item(e, pix, cbase, slot[q]);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const int ci = cbase + j;
+                        const int off = (pix >= 0 && ci < a.Cin) ? 2 * int(ci * plane + pix) : kOOBc;
+                        v[q].h[j] = __builtin_amdgcn_raw_buffer_load_b16(rin, off, 0, 0);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < kUB; ++q)
+                    if (slot[q] >= 0) *reinterpret_cast<uint4*>(pl + slot[q]) = v[q].v;
+            }
+        } else {
+            for (int e = tid; e < G * OB; e += kThreads) {
+                Pack8 p;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int64_t off = w_item(e, j);
+                    p.h[j] = off >= 0 ? w[off] : uint16_t(0);
+                }
+                *reinterpret_cast<uint4*>(wl + e * 8) = p.v;
+            }
+            for (int e = tid; e < PR * CCG * PC; e += kThreads) {
+                int64_t pix;
+                int cbase, slot;
+                p_item(e, pix, cbase, slot);
+                const uint16_t* src = in + pix;
+                Pack8 p;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int ci = cbase + j;
+                    p.h[j] = (pix >= 0 && ci < a.Cin) ? src[int64_t(ci) * plane] : uint16_t(0);
+                }
+                *reinterpret_cast<uint4*>(pl + slot) = p.v;
+            }
         }
         __syncthreads();
 
@@ -213,7 +277,7 @@ __global__ __launch_bounds__(kThreads) void igemm_bf16_kernel(IgemmArgs a) {
         }
 }
 
-template <int OB>
+template <int OB, bool RB>
 __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int NOB = OB / 32;
@@ -249,52 +313,106 @@ __global__ __launch_bounds__(kThreads) void igemm_f32_kernel(IgemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
+    const __amdgpu_buffer_rsrc_t rin = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(in), 0, RB ? int(a.Cin * plane * 4) : 0, kRWord3c);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(w), 0, RB ? a.wK * a.wC * a.R * a.S * 4 : 0, kRWord3c);
     for (int c0 = 0; c0 < a.Cin; c0 += CC) {
         __syncthreads();
-        for (int e = tid; e < KG * OB; e += kThreads) {
+        auto w_item = [&](int e) -> int64_t {   // element offset of weight item e, or -1
             const int kg = e / OB, ol = e - kg * OB;
             const int t = kg / CC, cl = kg - t * CC;
             const int tr = t / a.Ts, ts = t - tr * a.Ts;
             const int o = o0 + ol, ci = c0 + cl;
             const int wr = a.wr0 + a.wrstep * tr, ws = a.ws0 + a.wsstep * ts;
-            wl[e] = (o < a.Cout && ci < a.Cin) ? w[o * a.w_os + ci * a.w_cs + wr * a.S + ws] : 0.f;
-        }
-        for (int e = tid; e < CC * PR * PC; e += kThreads) {
+            return (o < a.Cout && ci < a.Cin) ? o * a.w_os + ci * a.w_cs + wr * a.S + ws : -1;
+        };
+        auto p_item = [&](int e, int& slot) -> int64_t {   // element offset of patch item e, or -1
             const int pc = e % PC;
             const int rest = e / PC;
             const int pr = rest % PR, cl = rest / PR;
             const int gr = row_in0 + pr, gc = col_in0 + pc, ci = c0 + cl;
             const bool ok = gr >= 0 && gr < a.in_rows && gc >= 0 && gc < a.in_cols && ci < a.Cin;
-            pl[cl * PLN + pr * PC + pc] = ok ? in[int64_t(ci) * plane + int64_t(gr) * a.in_pitch + gc] : 0.f;
+            slot = cl * PLN + pr * PC + pc;
+            return ok ? ci * plane + int64_t(gr) * a.in_pitch + gc : -1;
+        };
+        if constexpr (RB) {
+            const int nw = KG * OB, np = CC * PR * PC;
+            for (int e0 = tid; e0 < nw; e0 += kThreads * kUF) {
+                float v[kUF];
+#pragma unroll
+                for (int q = 0; q < kUF; ++q) {
+                    // past the end: an out-of-range load, no memory access
+                    const int64_t off = e0 + q * kThreads < nw ? w_item(e0 + q * kThreads) : -1;
+                    v[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                        rw, off >= 0 ? 4 * int(off) : kOOBc, 0, 0));
+                }
+#pragma unroll
+                for (int q = 0; q < kUF; ++q)
+                    if (e0 + q * kThreads < nw) wl[e0 + q * kThreads] = v[q];
+            }
+            for (int e0 = tid; e0 < np; e0 += kThreads * kUF) {
+                float v[kUF];
+                int slot[kUF];
+#pragma unroll
+                for (int q = 0; q < kUF; ++q) {
+                    const int e = e0 + q * kThreads;
+                    int64_t off = -1;   // past the end: an out-of-range load, no memory access
+                    slot[q] = -1;
+                    if (e < np) off = p_item(e, slot[q]);
+                    v[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                        rin, off >= 0 ? 4 * int(off) : kOOBc, 0, 0));
+                }
+#pragma unroll
+                for (int q = 0; q < kUF; ++q)
+                    if (slot[q] >= 0) pl[slot[q]] = v[q];
+            }
+        } else {
+            for (int e = tid; e < KG * OB; e += kThreads) {
+                const int64_t off = w_item(e);
+                wl[e] = off >= 0 ? w[off] : 0.f;
+            }
+            for (int e = tid; e < CC * PR * PC; e += kThreads) {
+                int slot;
+                const int64_t off = p_item(e, slot);
+                pl[slot] = off >= 0 ? in[off] : 0.f;
+            }
         }
         __syncthreads();
 
-        const int nk = (KG + 1) / 2;
-        for (int k = 0; k < nk; ++k) {
-            const int kg = 2 * k + hi;
+        // k-steps: (tap t, channel pair c2) with t-major order, channels 2 c2
+        // (lanes 0-31) and 2 c2 + 1 (lanes 32-63); CC is even, so a step's
+        // two channels share the tap.  The tap and its (tr, ts) advance
+        // incrementally, four steps per pass so that their operand reads can
+        // be issued ahead of the MFMAs.
+        const int CCH = CC / 2, nk = Tt * CCH;
+        int c2 = 0, t = 0, tr = 0, ts = 0;
+        auto kstep = [&]() __attribute__((always_inline)) {
+            const int cl = 2 * c2 + hi, kg = t * CC + cl;
             float A[NOB], B[2];
-            if (kg < KG) {
-                const int t = kg / CC, cl = kg - t * CC;
-                const int tr = t / a.Ts, ts = t - tr * a.Ts;
 #pragma unroll
-                for (int ob = 0; ob < NOB; ++ob) A[ob] = wl[kg * OB + ob * 32 + l32];
+            for (int ob = 0; ob < NOB; ++ob) A[ob] = wl[kg * OB + ob * 32 + l32];
 #pragma unroll
-                for (int pb = 0; pb < 2; ++pb) {
-                    const int pm = (pb * 32 + l32) * a.istr, pw = wave * a.istr;
-                    const int prow = (cm ? pm : pw) + tr, pcol = (cm ? pw : pm) + ts;
-                    B[pb] = pl[cl * PLN + prow * PC + pcol];
-                }
-            } else {
-#pragma unroll
-                for (int ob = 0; ob < NOB; ++ob) A[ob] = 0.f;
-                B[0] = B[1] = 0.f;
+            for (int pb = 0; pb < 2; ++pb) {
+                const int pm = (pb * 32 + l32) * a.istr, pw = wave * a.istr;
+                const int prow = (cm ? pm : pw) + tr, pcol = (cm ? pw : pm) + ts;
+                B[pb] = pl[cl * PLN + prow * PC + pcol];
             }
 #pragma unroll
             for (int ob = 0; ob < NOB; ++ob)
 #pragma unroll
                 for (int pb = 0; pb < 2; ++pb)
                     acc[ob][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(A[ob], B[pb], acc[ob][pb], 0, 0, 0);
-        }
+            const bool wrap = ++c2 == CCH;
+            c2 = wrap ? 0 : c2;
+            t += wrap ? 1 : 0;
+            const bool rwrap = wrap && ++ts == a.Ts;
+            ts = rwrap ? 0 : ts;
+            tr += rwrap ? 1 : 0;
+        };
+        int k = 0;
+        for (; k + 4 <= nk; k += 4) { kstep(); kstep(); kstep(); kstep(); }
+        for (; k < nk; ++k) kstep();
     }
 
     float* out = a.out + tile * a.out_tile + int64_t(n) * a.Cout * a.out_rows * a.out_cols;
@@ -369,9 +487,14 @@ bool igemm_plan(IgemmArgs& a, int dtype) {
     cands[nc++] = std::min(cin_r, maxcc);
     for (int c = maxcc; c >= gran; c /= 2)
         if (c < cands[0]) cands[nc++] = c;
-    // prefer two workgroups per CU (<= 80 KB of LDS), else the device limit
+    // prefer two workgroups per CU (<= 80 KB of LDS), else the device limit;
+    // a grid of at most one workgroup per CU takes the widest chunk the
+    // device allows (fewer chunks: fewer staging rounds and barriers)
     const int limit = device_lds_limit();
-    for (int budget : {std::min(80 * 1024, limit), limit}) {
+    const int64_t nwg = int64_t(a.frame ? a.fblk[a.fseg] : ((a.Vo + kBW - 1) / kBW) * ((a.Uo + kBH - 1) / kBH)) *
+                        ((a.Cout + a.OB - 1) / a.OB) * a.ntiles * a.Nn;
+    const int small = nwg <= device_cu_count() ? limit : std::min(80 * 1024, limit);
+    for (int budget : {small, limit}) {
         for (int i = 0; i < nc; ++i) {
             const int b = lds_bytes_for(a, dtype, cands[i], a.OB);
             if (b <= budget) {
@@ -393,32 +516,28 @@ hipError_t launch_igemm(const IgemmArgs& a, int dtype, hipStream_t s) {
     dim3 grid(a.frame ? a.fblk[a.fseg] : nvb * nub, (a.Cout + a.OB - 1) / a.OB, a.ntiles * a.Nn);
     if (grid.x == 0) return hipSuccess;   // an empty frame
     dim3 block(kThreads);
+    // buffer loads when the sample's input and the weights are under 2^31 bytes
+    const int64_t es = dtype == 1 ? 2 : 4;
+    const bool rb = int64_t(a.Cin) * a.in_rows * a.in_pitch * es < kOOBc &&
+                    int64_t(a.wK) * a.wC * a.R * a.S * es < kOOBc;
+    const void* f;
+    if (dtype == 1)
+        f = a.OB == 32 ? (rb ? reinterpret_cast<const void*>(igemm_bf16_kernel<32, true>)
+                             : reinterpret_cast<const void*>(igemm_bf16_kernel<32, false>))
+                       : (rb ? reinterpret_cast<const void*>(igemm_bf16_kernel<64, true>)
+                             : reinterpret_cast<const void*>(igemm_bf16_kernel<64, false>));
+    else
+        f = a.OB == 32 ? (rb ? reinterpret_cast<const void*>(igemm_f32_kernel<32, true>)
+                             : reinterpret_cast<const void*>(igemm_f32_kernel<32, false>))
+                       : (rb ? reinterpret_cast<const void*>(igemm_f32_kernel<64, true>)
+                             : reinterpret_cast<const void*>(igemm_f32_kernel<64, false>));
     if (a.lds_bytes > 64 * 1024) {
-        hipError_t e = hipSuccess;
-        if (dtype == 1)
-            e = a.OB == 32 ? hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_bf16_kernel<32>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes)
-                           : hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_bf16_kernel<64>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
-        else
-            e = a.OB == 32 ? hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_f32_kernel<32>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes)
-                           : hipFuncSetAttribute(reinterpret_cast<const void*>(igemm_f32_kernel<64>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
+        hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
         if (e != hipSuccess) return e;
     }
-    if (dtype == 1) {
-        if (a.OB == 32)
-            hipLaunchKernelGGL(igemm_bf16_kernel<32>, grid, block, a.lds_bytes, s, a);
-        else
-            hipLaunchKernelGGL(igemm_bf16_kernel<64>, grid, block, a.lds_bytes, s, a);
-    } else {
-        if (a.OB == 32)
-            hipLaunchKernelGGL(igemm_f32_kernel<32>, grid, block, a.lds_bytes, s, a);
-        else
-            hipLaunchKernelGGL(igemm_f32_kernel<64>, grid, block, a.lds_bytes, s, a);
-    }
-    return hipGetLastError();
+    IgemmArgs ak = a;
+    void* args[] = {&ak};
+    return hipLaunchKernel(f, grid, block, args, a.lds_bytes, s);
 }
 
 }  // namespace dc

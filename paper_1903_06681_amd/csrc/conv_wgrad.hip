@@ -1066,7 +1066,30 @@ __global__ __launch_bounds__(kThreads) void wgrad_rows_bf16_kernel(WgradArgs a) 
 
 // ---------------------------------------------------------------- fp32
 
-template <int NBW>
+// RB: the tile's x and dy are under 2^31 bytes: the staging gathers are
+// buffer loads (an element past the tile or the filters is an offset past
+// the buffer's end, which reads zero) issued kRF per thread before the first
+// wait; otherwise one load round trip per element.
+static constexpr int kRF = 8;
+static constexpr int kRFWord3 = 0x00020000;   // buffer resource word 3 (gfx9 family: raw access)
+static constexpr int kRFOOB = 0x7fffffff;     // byte offset past every buffer here: the load returns 0
+
+// n / d and n % d (0 <= n < 2^22, d >= 1) from a float reciprocal of d: the
+// product is within one of the quotient, which one correction each way
+// makes exact.
+__device__ __forceinline__ int rf_divmod(int n, int d, float inv, int& r) {
+    int q = int(float(n) * inv);
+    r = n - q * d;
+    const bool lo = r < 0;
+    q -= lo ? 1 : 0;
+    r += lo ? d : 0;
+    const bool hi = r >= d;
+    q += hi ? 1 : 0;
+    r -= hi ? d : 0;
+    return q;
+}
+
+template <int NBW, bool RB>
 __global__ __launch_bounds__(kThreads) void wgrad_rows_f32_kernel(WgradArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int DYP = kBQ + 1;
@@ -1110,6 +1133,11 @@ __global__ __launch_bounds__(kThreads) void wgrad_rows_f32_kernel(WgradArgs a) {
     const int64_t xplane = int64_t(a.x_rows) * a.x_pitch;
     const int dy_rows = a.Hot + 2 * a.dy_off;
     const int64_t dyplane = int64_t(dy_rows) * a.dy_pitch;
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(xt), 0, RB ? int(int64_t(a.Nn) * a.C * xplane * 4) : 0, kRFWord3);
+    const __amdgpu_buffer_rsrc_t rdy = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(dyt), 0, RB ? int(int64_t(a.Nn) * a.K * dyplane * 4) : 0, kRFWord3);
+    const float inv_xw = 1.0f / float(XW), inv_r = 1.0f / float(a.R);
 
     floatx16 acc[2][NBW];
 #pragma unroll
@@ -1125,25 +1153,68 @@ __global__ __launch_bounds__(kThreads) void wgrad_rows_f32_kernel(WgradArgs a) {
         for (int cb = 0; cb < ncb; ++cb) {
             const int q0 = cb * kBQ;
             __syncthreads();
-            for (int e = tid; e < 64 * kBQ; e += kThreads) {
-                const int q = e % kBQ, ol = e / kBQ;
-                const int o = o0 + ol;
-                float v = 0.f;
-                if (o < a.K && q0 + q < a.Wot)
-                    v = dyt[(int64_t(n) * a.K + o) * dyplane + int64_t(p + a.dy_off) * a.dy_pitch +
-                            a.dy_off + q0 + q];
-                dyl[ol * DYP + q] = v;
-            }
-            for (int e = tid; e < span * a.R * XW; e += kThreads) {
-                const int xc = e % XW;
-                const int rest = e / XW;
-                const int r = rest % a.R, cl = rest / a.R;
-                const int gr = p * a.istr + a.base_r + r;
-                const int gc = q0 * a.istr + a.base_c + xc;
-                float v = 0.f;
-                if (gr < a.x_rows && gc < a.x_cols)
-                    v = xt[(int64_t(n) * a.C + ci_lo + cl) * xplane + int64_t(gr) * a.x_pitch + gc];
-                xl[e] = v;
+            if constexpr (RB) {
+                for (int e0 = tid; e0 < 64 * kBQ; e0 += kThreads * kRF) {
+                    float v[kRF];
+#pragma unroll
+                    for (int u = 0; u < kRF; ++u) {
+                        const int e = e0 + u * kThreads;
+                        const int q = e % kBQ, ol = e / kBQ;
+                        const int o = o0 + ol;
+                        const bool ok = e < 64 * kBQ && o < a.K && q0 + q < a.Wot;
+                        const int off = ok ? 4 * int((int64_t(n) * a.K + o) * dyplane +
+                                                     int64_t(p + a.dy_off) * a.dy_pitch + a.dy_off + q0 + q)
+                                           : kRFOOB;
+                        v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rdy, off, 0, 0));
+                    }
+#pragma unroll
+                    for (int u = 0; u < kRF; ++u) {
+                        const int e = e0 + u * kThreads;
+                        if (e < 64 * kBQ) dyl[(e / kBQ) * DYP + e % kBQ] = v[u];
+                    }
+                }
+                const int nx = span * a.R * XW;
+                for (int e0 = tid; e0 < nx; e0 += kThreads * kRF) {
+                    float v[kRF];
+#pragma unroll
+                    for (int u = 0; u < kRF; ++u) {
+                        const int e = e0 + u * kThreads;
+                        int xc, r;
+                        const int rest = rf_divmod(e, XW, inv_xw, xc);
+                        const int cl = rf_divmod(rest, a.R, inv_r, r);
+                        const int gr = p * a.istr + a.base_r + r;
+                        const int gc = q0 * a.istr + a.base_c + xc;
+                        const bool ok = e < nx && gr < a.x_rows && gc < a.x_cols;
+                        const int off = ok ? 4 * int((int64_t(n) * a.C + ci_lo + cl) * xplane +
+                                                     int64_t(gr) * a.x_pitch + gc)
+                                           : kRFOOB;
+                        v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rx, off, 0, 0));
+                    }
+#pragma unroll
+                    for (int u = 0; u < kRF; ++u)
+                        if (e0 + u * kThreads < nx) xl[e0 + u * kThreads] = v[u];
+                }
+            } else {
+                for (int e = tid; e < 64 * kBQ; e += kThreads) {
+                    const int q = e % kBQ, ol = e / kBQ;
+                    const int o = o0 + ol;
+                    float v = 0.f;
+                    if (o < a.K && q0 + q < a.Wot)
+                        v = dyt[(int64_t(n) * a.K + o) * dyplane + int64_t(p + a.dy_off) * a.dy_pitch +
+                                a.dy_off + q0 + q];
+                    dyl[ol * DYP + q] = v;
+                }
+                for (int e = tid; e < span * a.R * XW; e += kThreads) {
+                    const int xc = e % XW;
+                    const int rest = e / XW;
+                    const int r = rest % a.R, cl = rest / a.R;
+                    const int gr = p * a.istr + a.base_r + r;
+                    const int gc = q0 * a.istr + a.base_c + xc;
+                    float v = 0.f;
+                    if (gr < a.x_rows && gc < a.x_cols)
+                        v = xt[(int64_t(n) * a.C + ci_lo + cl) * xplane + int64_t(gr) * a.x_pitch + gc];
+                    xl[e] = v;
+                }
             }
             __syncthreads();
             if (!wave_active) continue;
@@ -1589,9 +1660,18 @@ hipError_t launch_wgrad(const WgradArgs& a, int dtype, hipStream_t s) {
             default: return hipErrorInvalidValue;
         }
     } else {
-        e = set_lds(wgrad_rows_f32_kernel<2>, a.lds_bytes);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(wgrad_rows_f32_kernel<2>, grid, dim3(kThreads), a.lds_bytes, s, a);
+        // buffer loads when the tile's x and dy are under 2^31 bytes
+        const int64_t xb = int64_t(a.Nn) * a.C * a.x_rows * a.x_pitch * 4;
+        const int64_t dyb = int64_t(a.Nn) * a.K * (a.Hot + 2 * a.dy_off) * a.dy_pitch * 4;
+        if (xb < kRFOOB && dyb < kRFOOB) {
+            e = set_lds(wgrad_rows_f32_kernel<2, true>, a.lds_bytes);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL((wgrad_rows_f32_kernel<2, true>), grid, dim3(kThreads), a.lds_bytes, s, a);
+        } else {
+            e = set_lds(wgrad_rows_f32_kernel<2, false>, a.lds_bytes);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL((wgrad_rows_f32_kernel<2, false>), grid, dim3(kThreads), a.lds_bytes, s, a);
+        }
         e = hipGetLastError();
     }
     if (e != hipSuccess) return e;

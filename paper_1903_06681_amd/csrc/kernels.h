@@ -97,6 +97,8 @@ struct IgemmArgs {
 
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
 int device_lds_limit();
+// Compute units of the current device.
+int device_cu_count();
 
 // Frame mode: the output rows above / below and columns left / right of the
 // interior, of widths bands[0..3] (clamped to the Uo x Vo output), as the
