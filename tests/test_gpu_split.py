@@ -55,6 +55,10 @@ LAYERS = {
     # fp32 frame kernel: 5x5 (the runtime instantiation), 40 channels in
     # chunks of 16 (the last one partial), 24 output channels
     "f32k5": Layer("f32k5", 1, 40, 24, 40, 48, 5, 5, 1, 2, 2, 2, 2, "f32", "uniform", 209),
+    # 5x5 tiles with three-wide bands: the frame is the whole tile (bottom
+    # rows clamped, no side segments)
+    "tiny7": Layer("tiny7", 2, 8, 8, 10, 10, 7, 7, 1, 3, 2, 2, 3, "bf16", "uniform", 210),
+    "tiny7f": Layer("tiny7f", 2, 8, 8, 10, 10, 7, 7, 1, 3, 2, 2, 3, "f32", "uniform", 211),
 }
 
 
