@@ -186,7 +186,10 @@ dc_status dc_conv_bwd_filter_noalloc(const dc_problem* prob, int32_t tile, const
  * owned block of t_pad (which = DC_X: an x tile; DC_DY: a dy tile) that each
  * existing neighbour needs into the send buffer.  Reads only the owned block
  * (and pitch columns, see above); writes only regions whose neighbour
- * exists.  Bitwise copy.
+ * exists.  Bitwise copy.  When dc_halo_elems is 0 (every band empty: a
+ * margin no pass reads, e.g. a 1x1 filter) send may be NULL and nothing is
+ * launched; for dc_halo_unpack recv may then be NULL, and the call only
+ * zero-fills the margin ring.
  */
 dc_status dc_halo_pack(const dc_problem* prob, int32_t tile, int32_t which,
                        const void* t_pad, void* send, void* stream);

@@ -171,8 +171,15 @@ static dc_status halo_common(const dc_problem* prob, int32_t tile, int32_t which
     const int ch = x ? g.C : g.K;
     const int Ht = x ? g.Ht : g.Hot, Wt = x ? g.Wt : g.Wot;
     if (g.h == 0) return DC_OK;  // K = 1: no margin at all (Sec. III-A)
-    if (!src || !dst) return DC_ERR_NULL;
-    if (misaligned(src) || misaligned(dst)) return DC_ERR_ALIGN;
+    // the packed buffer (send of a pack, recv of an unpack) may be null when
+    // every band is empty (a margin that no pass reads): there is nothing to
+    // send, and the unpack only zero-fills the margin ring
+    const bool empty = (x ? g.x_halo : g.dy_halo) == 0;
+    const void* packed = unpack ? src : dst;
+    const void* tile_pad = unpack ? dst : src;
+    if (!tile_pad || (!packed && !empty)) return DC_ERR_NULL;
+    if (misaligned(tile_pad) || (packed && misaligned(packed))) return DC_ERR_ALIGN;
+    if (empty && !unpack) return DC_OK;
     HaloArgs a;
     std::memset(&a, 0, sizeof(a));
     a.src = src; a.dst = dst;

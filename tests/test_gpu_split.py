@@ -59,6 +59,9 @@ LAYERS = {
     # rows clamped, no side segments)
     "tiny7": Layer("tiny7", 2, 8, 8, 10, 10, 7, 7, 1, 3, 2, 2, 3, "bf16", "uniform", 210),
     "tiny7f": Layer("tiny7f", 2, 8, 8, 10, 10, 7, 7, 1, 3, 2, 2, 3, "f32", "uniform", 211),
+    # 1x1 filter: no band, an empty frame (the boundary call launches nothing)
+    "k1": Layer("k1", 2, 16, 24, 32, 48, 1, 1, 1, 0, 2, 2, 1, "bf16", "uniform", 212),
+    "k1f": Layer("k1f", 2, 16, 24, 32, 48, 1, 1, 1, 0, 2, 2, 1, "f32", "uniform", 213),
 }
 
 

@@ -106,6 +106,21 @@ def test_one_by_one_needs_no_halo_and_packs_nothing():
     dc.halo_unpack(p, dc.DC_ALL_TILES, dc.DC_X, A16, A32, 0)
 
 
+def test_empty_bands_accept_a_null_packed_buffer():
+    """A margin no pass reads (1x1 filter with h = 1): every band is empty, so
+    the send buffer of a pack may be NULL and nothing is launched; the tile
+    pointer is still required, and a non-empty halo still requires both."""
+    p = prob(R=1, S=1, pad=0, halo=1)
+    assert dc.halo_elems(p, dc.DC_X) == 0 and dc.halo_elems(p, dc.DC_DY) == 0
+    dc.halo_pack(p, dc.DC_ALL_TILES, dc.DC_X, A16, None, 0)
+    dc.halo_pack(p, 0, dc.DC_DY, A16, None, 0)
+    assert _status(dc.halo_pack, p, 0, dc.DC_X, None, None, 0) == -1
+    assert _status(dc.halo_unpack, p, 0, dc.DC_X, None, None, 0) == -1
+    q = prob()
+    assert dc.halo_elems(q, dc.DC_X) > 0
+    assert _status(dc.halo_pack, q, 0, dc.DC_X, A16, None, 0) == -1
+
+
 @pytest.mark.parametrize("R,S,stride,pad,H,W,P,Q", [
     (3, 3, 1, 1, 32, 32, 2, 2), (5, 5, 1, 2, 40, 40, 4, 4), (1, 1, 1, 0, 16, 16, 2, 2),
     (7, 7, 2, 3, 224, 224, 2, 2), (3, 3, 2, 1, 32, 32, 2, 2), (7, 7, 2, 3, 64, 64, 4, 4),
