@@ -132,6 +132,9 @@ SMALL = {
     # past the largest class, on the chunked and row kernels instead
     "f32_c1": Layer("f32_c1", 2, 1, 3, 20, 24, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 114),
     "f32_c36": Layer("f32_c36", 1, 36, 40, 24, 24, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 115),
+    # a single filter (K = 1): one-channel input-gradient reduction, one-row weight gradient
+    "k_one": Layer("k_one", 2, 16, 1, 24, 40, 3, 3, 1, 1, 2, 2, 1, "bf16", "uniform", 116),
+    "k_one_f32": Layer("k_one_f32", 2, 5, 1, 20, 28, 3, 3, 1, 1, 2, 2, 1, "f32", "uniform", 117),
 }
 
 
@@ -184,7 +187,8 @@ def test_small_layer_all_tiles_matches_undecomposed_oracle(name):
                                   "s2ph5_bf16", "kslice_bf16", "kslice_p0_bf16", "bp7_bf16", "bp3_bf16",
                                   "roll_bf16", "roll96_bf16", "roll5_bf16", "roll5b_bf16",
                                   "roll50_bf16", "roll5c_bf16", "roll5d_bf16", "roll5e_bf16",
-                                  "f32_c3", "f32_c17", "k1_c22_f32", "f32_c1", "f32_c36"])
+                                  "f32_c3", "f32_c17", "k1_c22_f32", "f32_c1", "f32_c36", "k_one",
+                                  "k_one_f32"])
 def test_integer_inputs_are_bit_exact(name):
     """Integer data in {-2..2}: all sums are exact integers, whatever the order."""
     L = SMALL[name]
