@@ -12,7 +12,8 @@ not reach on their own:
 * the benchmark's two-stream step (the dy halo exchange beside the weight
   gradient, Sec. IV-A) equals the one-stream step bit for bit;
 * the interior / boundary split (Sec. IV-A) on the c5a, c5b and c4 tiles
-  equals the whole-tile passes bit for bit on integer-valued inputs.
+  (and c5a's corner tile) equals the whole-tile passes bit for bit on
+  integer-valued inputs.
 """
 import numpy as np
 import pytest
@@ -174,17 +175,17 @@ def test_two_stream_step_equals_one_stream_step():
     assert torch.equal(_bits(dyp_nan), _bits(dyp))
 
 
-@pytest.mark.parametrize("name", ["c5a", "c5b", "c4"])
-def test_full_size_split_equals_whole_tile(name):
+@pytest.mark.parametrize("name,tile", [("c5a", 5), ("c5a", 0), ("c5b", 5), ("c4", 5)])
+def test_full_size_split_equals_whole_tile(name, tile):
     """The split step of the benchmark on an interior tile at full size (c5a:
     the benchmark's; c5b: 5x5, bands two wide; c4: fp32): forward and input
     gradient on the interior while every margin still holds NaN, then the
     boundary frames once the margins are filled, equal the whole-tile passes
-    bit for bit.  Inputs are integers in [-2, 2]: every sum is exact in fp32,
+    bit for bit (tile 0 of c5a: a corner, whose frame reads the zero padding
+    on two sides).  Inputs are integers in [-2, 2]: every sum is exact in fp32,
     so the frame kernels' order of additions and the whole-tile kernels' give
     the same bits."""
     L = wl.LAYERS[name]
-    tile = 5
     print(f"[split full] {name} tile {tile}, integer inputs", flush=True)
     p, wd, xp, dyp, dyp_nan, _, _ = _tile_setup(L, tile, dist="int")
     h = L.halo
